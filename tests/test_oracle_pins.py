@@ -1,0 +1,461 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than its own formula: a
+closed form, a brute-force enumeration, an invariant the paper states, a
+textbook special case or a value the paper prints.  Each is chosen so that a
+plausible slip (a dropped term, a window off by one, a wrong variance
+estimator, a sign flipped, a tie broken the wrong way) fails it.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.stats import spearmanr
+
+import oracle as O
+import synth
+
+W = 64
+EPS = 1e-6
+
+
+# ---------------------------------------------------------------------------
+# bf16 widening (format definition)
+# ---------------------------------------------------------------------------
+def test_bf16_widening_known_patterns():
+    bits = np.array([0x3F80, 0xC000, 0x7F80, 0xFF80, 0x0000, 0x8000, 0x4049,
+                     0x0001, 0x3F81], dtype=np.uint16)
+    v = O.bf16_to_float64(bits)
+    assert v[0] == 1.0 and v[1] == -2.0
+    assert v[2] == math.inf and v[3] == -math.inf
+    assert v[4] == 0.0 and math.copysign(1.0, v[5]) == -1.0
+    assert v[6] == 3.140625                      # 0x4049 = 1.5703125 * 2
+    assert v[7] == 2.0 ** -133                   # smallest bf16 subnormal
+    assert v[8] == 1.0 + 2.0 ** -7               # one ulp above 1 in bf16
+    assert np.isnan(O.bf16_to_float64(np.array([0x7FC0], np.uint16)))[0]
+
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    g = synth.rng(11)
+    x = (g.standard_normal(20000) * 10.0 ** g.integers(-30, 30, 20000)
+         ).astype(np.float32)
+    x[:4] = [np.inf, -np.inf, 0.0, -0.0]
+    ours = synth.f32_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy()
+    assert np.array_equal(ours, ref.view(np.uint16))
+    # round trip through the oracle's widening is the identity on bf16 values
+    back = O.bf16_to_float64(ours).astype(np.float32)
+    assert np.array_equal(synth.f32_to_bf16_bits(back), ours)
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1: g_l(t) = || h_l(t) - h_l(t-1) ||_2
+# ---------------------------------------------------------------------------
+def test_residual_delta_axis_steps():
+    D = 16
+    h = np.zeros((4, D))
+    h[1, 3] = 2.5          # step along one axis
+    h[2, 3] = 2.5
+    h[2, 7] = -4.0         # second step along another axis
+    h[3] = h[2]            # no change
+    g, has = O.residual_delta(h, np.zeros(D))
+    assert has.all()
+    assert g.tolist() == [0.0, 2.5, 4.0, 0.0]
+
+
+def test_residual_delta_pythagorean_triples():
+    h = np.zeros((4, 3))
+    h[1] = [3.0, 4.0, 0.0]          # |(3,4,0)| = 5
+    h[2] = [4.0, 6.0, 2.0]          # |(1,2,2)| = 3
+    h[3] = [6.0, 9.0, 8.0]          # |(2,3,6)| = 7
+    g, _ = O.residual_delta(h, np.zeros(3))
+    assert g.tolist() == [0.0, 5.0, 3.0, 7.0]
+
+
+def test_residual_delta_is_norm_of_difference_not_difference_of_norms():
+    x = np.array([1.0, 2.0, 2.0])   # |x| = 3
+    h = np.stack([x, -x])
+    g, _ = O.residual_delta(h, x)   # first row equals its predecessor
+    assert g.tolist() == [0.0, 6.0]
+
+
+def test_residual_delta_stream_start_has_no_sample():
+    h = np.ones((3, 5))
+    g, has = O.residual_delta(h, None)
+    assert has.tolist() == [False, True, True]
+    assert g[1] == 0.0
+
+
+# ---------------------------------------------------------------------------
+# Eq. 3: rolling z-score over a trailing window of w = 64 samples
+# ---------------------------------------------------------------------------
+def test_zscore_linear_ramp_closed_form():
+    # For x = a + c t with c > 0 every full window gives
+    # z = sqrt(3 (w-1) / (w+1)) (inclusive window, population sigma).
+    # An exclusive window or ddof=1 give 1.7593 / 1.6918 instead.
+    for a, c in [(0.0, 1.0), (1e3, 0.25), (-7.0, 3.0)]:
+        x = a + c * np.arange(300, dtype=np.float64)
+        z = O.rolling_zscore(x, W, EPS)
+        zc = math.sqrt(3.0 * (W - 1) / (W + 1))
+        sigma = c * math.sqrt((W * W - 1) / 12.0)
+        assert np.allclose(z[W - 1:], zc * sigma / (sigma + EPS),
+                           rtol=1e-12, atol=0)
+        assert abs(zc - 1.705196) < 1e-6
+
+
+def test_zscore_isolated_spike_closed_form():
+    # w-1 zeros then a value x: mu = x/w, sigma = x sqrt(w-1)/w, so
+    # z = sqrt(w-1) (= 7.937 at w = 64) for any x > 0.
+    for x in [1.0, 5.0, 1e4]:
+        s = np.zeros(W)
+        s[-1] = x
+        z = O.rolling_zscore(s, W, EPS)[-1]
+        sigma = x * math.sqrt(W - 1) / W
+        assert z == pytest.approx((x - x / W) / (sigma + EPS), rel=1e-13)
+        assert z == pytest.approx(math.sqrt(W - 1), rel=1e-5)
+
+
+def test_zscore_window_length_is_exactly_w():
+    g = synth.rng(5)
+    x = g.standard_normal(400)
+    base = O.rolling_zscore(x, W, EPS)
+    t = 300
+    y = x.copy()
+    y[t - W] += 100.0          # just outside the window of t
+    assert O.rolling_zscore(y, W, EPS)[t] == base[t]
+    y = x.copy()
+    y[t - W + 1] += 100.0      # oldest sample inside the window of t
+    assert O.rolling_zscore(y, W, EPS)[t] != base[t]
+
+
+def test_zscore_warmup():
+    z = O.rolling_zscore(np.array([4.0, 10.0, 10.0]), W, EPS)
+    assert z[0] == 0.0                                  # single sample
+    assert z[1] == pytest.approx(3.0 / (3.0 + EPS), rel=1e-14)  # two samples
+    # three samples {4, 10, 10}: mu = 8, sigma = sqrt(8), z = 2 / sqrt(8)
+    assert z[2] == pytest.approx(2.0 / (math.sqrt(8.0) + EPS), rel=1e-14)
+
+
+def test_zscore_constant_stream_is_zero():
+    assert np.all(O.rolling_zscore(np.full(200, 3.25), W, EPS) == 0.0)
+
+
+def test_zscore_affine_invariance():
+    g = synth.rng(6)
+    x = np.abs(g.standard_normal(500)) + 2.0
+    # eps = 0 so that the invariance is exact; the first sample (0/0) is
+    # left out.
+    z = O.rolling_zscore(x, W, 0.0)[1:]
+    for alpha, beta in [(3.0, 0.0), (0.01, 50.0), (250.0, -7.0)]:
+        assert np.allclose(O.rolling_zscore(alpha * x + beta, W, 0.0)[1:], z,
+                           atol=1e-9)
+    assert np.allclose(O.rolling_zscore(-2.0 * x + 1.0, W, 0.0)[1:], -z,
+                       atol=1e-9)
+
+
+def test_zscore_removes_positional_drift():
+    # Sec. 3.2: the raw signal tracks position; the causal z-score removes
+    # the trend.  Band A drifts down and Band B up (opposite signs).
+    g = synth.rng(7)
+    T = 4000
+    t = np.arange(T, dtype=np.float64)
+    a = g.standard_normal(T) + 10.0 - 0.004 * t
+    b = g.standard_normal(T) + 10.0 + 0.004 * t
+    raw = a - b
+    z = O.rolling_zscore(a, W, EPS) - O.rolling_zscore(b, W, EPS)
+    assert abs(spearmanr(raw[W:], t[W:])[0]) > 0.8
+    assert abs(spearmanr(z[W:], t[W:])[0]) < 0.05
+
+
+def test_zscore_is_causal_and_chunking_invariant():
+    g = synth.rng(8)
+    x = g.standard_normal(600)
+    full = O.rolling_zscore(x, W, EPS)
+    # appending future samples changes no earlier value
+    assert np.array_equal(O.rolling_zscore(x[:400], W, EPS), full[:400])
+    # processing in chunks with only the last w-1 samples carried over
+    out = []
+    prior = np.zeros(0)
+    for lo in range(0, 600, 128):
+        new = x[lo:lo + 128]
+        out.append(O.smooth_stream(prior, new, np.ones(new.size, bool),
+                                   O.SMOOTH_Z, W, EPS))
+        prior = np.concatenate([prior, new])[-(W - 1):]
+    assert np.array_equal(np.concatenate(out), full)
+
+
+def test_rolling_mean_ramp_closed_form():
+    x = 2.0 + 0.5 * np.arange(200, dtype=np.float64)
+    m = O.rolling_mean(x, W)
+    t = np.arange(W - 1, 200)
+    assert np.allclose(m[W - 1:], 2.0 + 0.5 * (t - (W - 1) / 2.0),
+                       rtol=1e-14)
+    assert m[0] == 2.0 and m[1] == 2.25
+
+
+def test_smooth_stream_skips_tokens_without_sample():
+    new = np.array([123.0, 1.0, 3.0])
+    out = O.smooth_stream(np.zeros(0), new, np.array([False, True, True]),
+                          O.SMOOTH_MEAN, W, EPS)
+    assert out.tolist() == [0.0, 1.0, 2.0]
+
+
+# ---------------------------------------------------------------------------
+# Band combination (Fig. 1, Eq. 3 text)
+# ---------------------------------------------------------------------------
+def test_band_score_reduces_to_z10_minus_z21():
+    g = synth.rng(9)
+    z = g.standard_normal((2, 50))
+    assert np.array_equal(O.band_score(z, 1, 1), z[0] - z[1])
+
+
+def test_band_score_signs():
+    base = np.zeros((15, 1))
+    up_a = base.copy()
+    up_a[3] = 1.0          # a Band A layer rises
+    up_b = base.copy()
+    up_b[10] = 1.0         # a Band B layer rises
+    assert O.band_score(up_a, 7, 8)[0] == pytest.approx(1.0 / 7.0)
+    assert O.band_score(up_b, 7, 8)[0] == pytest.approx(-1.0 / 8.0)
+    assert O.band_score(up_a, 15, 0)[0] == pytest.approx(1.0 / 15.0)
+
+
+def test_hs_chunk_scores_spike_on_band_a_raises_score():
+    # A token whose Band A hidden state jumps is scored above its
+    # neighbours; the same jump on Band B pushes it below (Sec. 3.2).
+    g = synth.rng(10)
+    n_a, n_b, T, D = 2, 2, 200, 32
+    hid = g.standard_normal((n_a + n_b, T, D))
+    prior = [np.zeros(0)] * 4
+    spike = 150
+    ha = hid.copy()
+    ha[:n_a, spike] *= 6.0
+    s_a, *_ = O.hs_chunk_scores(ha, None, prior, n_a, n_b)
+    assert np.argmax(s_a[W:]) + W == spike
+    hb = hid.copy()
+    hb[n_a:, spike] *= 6.0
+    s_b, *_ = O.hs_chunk_scores(hb, None, prior, n_a, n_b)
+    assert np.argmin(s_b[W:]) + W == spike
+
+
+# ---------------------------------------------------------------------------
+# Band constants against the paper's per-layer table (App. A)
+# ---------------------------------------------------------------------------
+def _rho_table():
+    path = os.path.join(os.path.dirname(__file__), "golden",
+                        "perlayer_rho.txt")
+    rows = [l.split() for l in open(path) if l.strip() and l[0] != "#"]
+    return {int(r[0]): [float(v) for v in r[1:]] for r in rows}
+
+
+def test_band_layers_have_the_sign_the_table_prints():
+    rho = _rho_table()
+    assert len(rho) == 32
+    for l in synth.BAND_A:
+        assert all(v > 0 for v in rho[l]), l
+    for l in synth.BAND_B:
+        assert all(v < 0 for v in rho[l]), l
+    # the layers just outside each band break its sign in some column
+    for l in (6, 14, 26):
+        assert not all(v > 0 for v in rho[l]) or not all(v < 0 for v in rho[l])
+    assert any(v < 0 for v in rho[6]) and any(v < 0 for v in rho[14])
+    assert any(v > 0 for v in rho[26])
+    # the last layer flips sign across columns and is not used
+    assert any(v > 0 for v in rho[31]) and any(v < 0 for v in rho[31])
+    # the single-layer preset 10/21 sits inside the bands
+    assert 10 in synth.BAND_A and 21 in synth.BAND_B
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.3: Lag-KV signal
+# ---------------------------------------------------------------------------
+def _lag_shapes(g, T=6, L=2, H=2, d=8):
+    return (g.standard_normal((T, L, H, d)), g.standard_normal((T, L, H, d)))
+
+
+def test_chunk_range_brute_force():
+    g = synth.rng(12)
+    k, v = _lag_shapes(g)
+    mn, mx = O.chunk_range(k, v)
+    T, L, H, d = k.shape
+    for l in range(L):
+        for h in range(H):
+            for c in range(d):
+                col_k = [k[t, l, h, c] for t in range(T)]
+                col_v = [v[t, l, h, c] for t in range(T)]
+                assert mn[l, 0, h, c] == min(col_k)
+                assert mx[l, 0, h, c] == max(col_k)
+                assert mn[l, 1, h, c] == min(col_v)
+                assert mx[l, 1, h, c] == max(col_v)
+
+
+def test_lagkv_previous_chunk_maps_into_unit_interval():
+    g = synth.rng(13)
+    k, v = _lag_shapes(g)
+    mn, mx = O.chunk_range(k, v)
+    kt = (k - mn[None, :, 0]) / (mx[None, :, 0] - mn[None, :, 0] + EPS)
+    assert kt.min() >= 0.0 and kt.max() < 1.0
+
+
+def test_lagkv_alternating_extremes_closed_form():
+    # A token whose channels alternate between the previous chunk's min and
+    # max normalises to 0,1,0,1,...: population variance 1/4 (times
+    # (r/(r+eps))^2), for K and V, so q = 1/2.
+    L, H, d = 2, 3, 8
+    mn = np.full((L, 2, H, d), -1.0)
+    mx = np.full((L, 2, H, d), 3.0)
+    tok = np.where(np.arange(d) % 2 == 0, -1.0, 3.0)
+    k = np.broadcast_to(tok, (1, L, H, d)).copy()
+    q = O.lagkv_signal(k, k.copy(), mn, mx, EPS)
+    r = 4.0 / (4.0 + EPS)
+    assert q[0] == pytest.approx(2 * 0.25 * r * r, rel=1e-14)
+    # a token at the middle of every range has zero variance
+    q0 = O.lagkv_signal(np.ones((1, L, H, d)), np.ones((1, L, H, d)), mn, mx)
+    assert q0[0] == 0.0
+
+
+def test_lagkv_invariant_to_per_channel_affine_maps():
+    # Sec. 3.3: the lag normalisation removes domain-level magnitude shifts.
+    g = synth.rng(14)
+    T, L, H, d = 5, 2, 2, 8
+    prev_k, prev_v = _lag_shapes(g, T, L, H, d)
+    k, v = _lag_shapes(g, T, L, H, d)
+    s_k = np.exp(g.standard_normal((L, H, d)))
+    o_k = g.standard_normal((L, H, d)) * 10
+    s_v = np.exp(g.standard_normal((L, H, d)))
+    o_v = g.standard_normal((L, H, d)) * 10
+    rng0 = O.chunk_range(prev_k, prev_v)
+    rng1 = O.chunk_range(prev_k * s_k + o_k, prev_v * s_v + o_v)
+    q0 = O.lagkv_signal(k, v, *rng0, eps=0.0)
+    q1 = O.lagkv_signal(k * s_k + o_k, v * s_v + o_v, *rng1, eps=0.0)
+    assert np.allclose(q0, q1, rtol=1e-10)
+
+
+def test_lagkv_first_chunk_uses_own_range():
+    g = synth.rng(15)
+    k, v = _lag_shapes(g)
+    s, q, own = O.lagkv_chunk_scores(k, v, None, np.zeros(0))
+    assert np.array_equal(q, O.lagkv_signal(k, v, *O.chunk_range(k, v)))
+    # the smoothed score of the first token is its own signal (one sample)
+    assert s[0] == q[0]
+
+
+# ---------------------------------------------------------------------------
+# Which positions survive (Sec. 3.1, Sec. 3.3, App. D)
+# ---------------------------------------------------------------------------
+def _dominates(scores, i, j):
+    """Position i outranks position j: higher score, or equal score and lower
+    position; NaN below everything (written independently of the oracle's
+    sort key)."""
+    si, sj = float(scores[i]), float(scores[j])
+    if math.isnan(si) and math.isnan(sj):
+        return i < j
+    if math.isnan(sj):
+        return True
+    if math.isnan(si):
+        return False
+    if si != sj:
+        return si > sj
+    return i < j
+
+
+def _brute_force_keep(scores, P, K, R):
+    N = len(scores)
+    if N <= K:
+        return list(range(N))
+    protected = set(range(P)) | set(range(N - R, N))
+    elig = [i for i in range(P, N - R)]
+    M = K - P - R
+    found = []
+    for sub in itertools.combinations(elig, M):
+        rest = [j for j in elig if j not in sub]
+        if all(_dominates(scores, i, j) for i in sub for j in rest):
+            found.append(sorted(protected | set(sub)))
+    assert len(found) == 1      # the retained set is unique
+    return found[0]
+
+
+def test_select_matches_brute_force_small():
+    g = synth.rng(16)
+    cases = 0
+    for N in range(1, 13):
+        for K in range(1, 13):
+            for P in range(0, 4):
+                R = K // 4
+                if N > K and P + R >= K:
+                    assert O.select_keep(np.zeros(N), P, K, R) == \
+                        O.BUDGET_ERROR
+                    continue
+                # coarse values force many exact ties
+                s = np.round(g.standard_normal(N) * 2) / 2
+                if N > 3:
+                    s[g.integers(0, N)] = np.nan
+                    s[g.integers(0, N)] = -0.0
+                got = O.select_keep(s, P, K, R)
+                assert got.tolist() == _brute_force_keep(s, P, K, R)
+                cases += 1
+    assert cases > 300
+
+
+def test_select_properties_large():
+    g = synth.rng(17)
+    for N, K, P in [(5000, 1024, 0), (5000, 1024, 37), (20000, 4096, 0)]:
+        s = synth.old_scores(g, N, ties=True)
+        keep = O.select_keep(s, P, K)
+        R = O.default_recent(K)
+        assert keep.size == K
+        assert np.all(np.diff(keep) > 0)
+        assert set(range(P)) <= set(keep.tolist())
+        assert set(range(N - R, N)) <= set(keep.tolist())
+        # every evicted eligible position is outranked by every kept one
+        kept_e = [i for i in keep if P <= i < N - R]
+        evicted = np.setdiff1d(np.arange(P, N - R), keep)
+        worst_kept = max(kept_e, key=lambda i: O.ranking_key(s[i], i))
+        best_evicted = min(evicted, key=lambda i: O.ranking_key(s[i], i))
+        assert _dominates(s, worst_kept, best_evicted)
+
+
+def test_select_ties_keep_lower_positions():
+    s = np.zeros(10)
+    keep = O.select_keep(s, 0, 6, 1)        # M = 5 of positions 0..8
+    assert keep.tolist() == [0, 1, 2, 3, 4, 9]
+
+
+def test_select_negative_zero_equals_zero_and_nan_is_lowest():
+    s = np.array([-0.0, 0.0, np.nan, -np.inf, 0.0, 5.0, 1.0])
+    keep = O.select_keep(s, 0, 5, 1)       # M = 4 of positions 0..5
+    assert keep.tolist() == [0, 1, 4, 5, 6]
+    keep = O.select_keep(s, 0, 6, 1)       # M = 5: -inf beats NaN
+    assert keep.tolist() == [0, 1, 3, 4, 5, 6]
+
+
+def test_select_no_eviction_and_budget_error():
+    assert O.select_keep(np.arange(8.0), 0, 8).tolist() == list(range(8))
+    assert O.select_keep(np.arange(3.0), 0, 8).tolist() == [0, 1, 2]
+    assert O.select_keep(np.arange(9.0), 6, 8) == O.BUDGET_ERROR   # 6+2>=8
+
+
+def test_default_recent():
+    assert O.default_recent(256) == 64
+    assert O.default_recent(4096) == 128
+    assert O.default_recent(8192) == 128
+    assert O.default_recent(100) == 25
+    assert O.default_recent(3) == 0
+
+
+# ---------------------------------------------------------------------------
+# App. H: order-preserving rebuild
+# ---------------------------------------------------------------------------
+def test_compact_rows_bytewise():
+    g = synth.rng(18)
+    rows = synth.random_bits16(g, (50, 4, 16))
+    rows[7, 0, 0] = 0x7FC1               # a NaN payload must survive
+    keep = np.array([0, 3, 7, 8, 20, 49])
+    out = O.compact_rows(rows, keep)
+    assert out.shape == (6, 4, 16)
+    for j, i in enumerate(keep):
+        assert out[j].tobytes() == rows[i].tobytes()
+    assert out[2, 0, 0] == 0x7FC1
