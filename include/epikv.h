@@ -1,0 +1,304 @@
+/*
+ * epikv.h -- C ABI of the EpiKV eviction step on AMD Instinct MI355X (gfx950).
+ *
+ * The step follows "Epiphany-Aware KV Cache Eviction Without the Attention
+ * Matrix" (Kolawole & Smith, arXiv 2606.26472):
+ *
+ *   score    hidden-state change g_l(t) = ||h_l(t) - h_l(t-1)||_2 at the band
+ *            layers (Sec. 3.2, Eq. 1), or the lag-normalised K/V variance
+ *            (Sec. 3.3, Lag-KV);
+ *   zscore   causal trailing-window smoothing (Eq. 3 z-score, or the Eq. 2
+ *            mean) and the band combination s = mean_A - mean_B (Fig. 1);
+ *            the result is the token's frozen score (Sec. 3.3);
+ *   select   keep the prefill, a recency window of R = min(128, K/4) and the
+ *            best scores so that exactly K positions survive (Sec. 3.1,
+ *            Sec. 3.3, App. D);
+ *   compact  rebuild the paged cache from the kept positions, in order, for
+ *            every layer, K and V and KV head (App. H; the cache holds
+ *            2*L*H*d_h scalars per token, Sec. 3.1).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are device pointers unless marked "host".  The caller owns
+ *   every buffer.  The library allocates nothing, keeps no global state,
+ *   never synchronises, and enqueues its kernels on `stream` (0 = the null
+ *   stream).  Calls on different streams are independent.
+ * - bf16 tensors are passed as raw 16-bit storage.
+ * - Return value: EPIKV_OK (0) or a negative epikv_status.  Every negative
+ *   code except EPIKV_ELAUNCH is detected on the host before anything is
+ *   enqueued, so a failed call leaves device memory untouched.
+ * - Per-sequence conditions that only the device sees (budget too small,
+ *   lengths or page ids out of range) are reported in seq_status[b] with an
+ *   epikv_seq_status value; the sequence's outputs are then left untouched.
+ */
+#ifndef EPIKV_H
+#define EPIKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Host-detected errors. */
+typedef enum epikv_status {
+  EPIKV_OK = 0,
+  EPIKV_EINVAL_NULL = -1,   /* a required pointer is NULL */
+  EPIKV_EINVAL_SHAPE = -2,  /* a size is out of the supported range */
+  EPIKV_EINVAL_PARAM = -3,  /* a parameter (budget, window, eps, enum) is invalid */
+  EPIKV_EALIGN = -4,        /* a pointer, stride or leading dimension is misaligned */
+  EPIKV_EWORKSPACE = -5,    /* workspace missing or smaller than required */
+  EPIKV_EALIAS = -6,        /* an output overlaps an input it must not overlap */
+  EPIKV_ELAUNCH = -7        /* the HIP runtime refused a kernel launch */
+} epikv_status;
+
+/* Per-sequence status written by the device. */
+typedef enum epikv_seq_status {
+  EPIKV_SEQ_OK = 0,
+  EPIKV_SEQ_BUDGET = 1,     /* N > K but P + R >= K: no room for scored tokens */
+  EPIKV_SEQ_RANGE = 2       /* N, P, a kept index or a page id out of range */
+} epikv_seq_status;
+
+/* Which per-token signal is scored. */
+typedef enum epikv_signal {
+  EPIKV_SIGNAL_HS = 0,      /* band-layer hidden-state change, Sec. 3.2 Eq. 1 */
+  EPIKV_SIGNAL_LAGKV = 1    /* lag-normalised key+value variance, Sec. 3.3 */
+} epikv_signal;
+
+/* How the per-token signal is smoothed over the trailing window. */
+typedef enum epikv_smoothing {
+  EPIKV_SMOOTH_Z = 0,       /* rolling z-score, Eq. 3 (EpiKV) */
+  EPIKV_SMOOTH_MEAN = 1,    /* rolling mean, Eq. 2 (HS-variance, KV family) */
+  EPIKV_SMOOTH_RAW = 2      /* no smoothing (App. E "raw") */
+} epikv_smoothing;
+
+#define EPIKV_MAX_BAND 32   /* band layers per call */
+#define EPIKV_MAX_WINDOW 256
+
+/*
+ * Configuration, passed by (host) pointer to every call.
+ *
+ * HS signal: n_band_a + n_band_b hidden-state layers are scored, Band A
+ * (positive weight) first.  The paper's bands are layers 7..13 (A) and
+ * 18..25 (B) of a 32-layer model (Sec. 3.2, App. A); the single-layer
+ * preset A = {10}, B = {21} gives Eq. 3's z_10 - z_21.  n_band_b may be 0.
+ * Lag-KV signal: one signal row per sequence, weight +1; the band fields
+ * are ignored.
+ */
+typedef struct epikv_cfg {
+  int32_t batch;        /* B >= 1 sequences */
+  int32_t hidden;       /* D: hidden width for the HS signal, 8..16384, D % 8 == 0 */
+  int32_t n_layers;     /* L: layers held in the KV pool, >= 1 */
+  int32_t n_kv_heads;   /* H >= 1 */
+  int32_t head_dim;     /* d: 64, 128 or 256; H*d <= 2048 */
+  int32_t page_size;    /* tokens per KV page, 1..1024 */
+  int32_t n_band_a;     /* HS: Band A layer count, >= 1 */
+  int32_t n_band_b;     /* HS: Band B layer count, >= 0; A + B <= EPIKV_MAX_BAND */
+  int32_t window;       /* w: trailing window in samples, 1..EPIKV_MAX_WINDOW (paper: 64) */
+  float eps;            /* epsilon added to sigma (Eq. 3) and to the Lag-KV range, >= 0 */
+  int32_t signal;       /* epikv_signal */
+  int32_t smoothing;    /* epikv_smoothing */
+  int32_t budget;       /* K >= 1: positions kept per sequence */
+  int32_t recent;       /* R >= 0, or -1 for min(128, K/4) (App. D) */
+} epikv_cfg;
+
+/*
+ * A paged bf16 KV pool.  The K (kv = 0) or V (kv = 1) row of the token in
+ * slot s of page p at layer l starts at
+ *     base + l*stride_layer + kv*stride_kv + p*stride_page + s*row_bytes
+ * with row_bytes = n_kv_heads*head_dim*2: all KV heads of one token are one
+ * contiguous row, heads outermost.  Strides are in bytes, multiples of 16,
+ * and base is 16-byte aligned.  Valid page ids are [0, n_pages).
+ */
+typedef struct epikv_pool {
+  void* base;
+  int64_t stride_layer;
+  int64_t stride_kv;
+  int64_t stride_page;
+  int64_t n_pages;
+} epikv_pool;
+
+/* Fill *cfg with the paper's setting: 32 layers, D = 4096, 8 KV heads x 128,
+ * 16-token pages, Band A = 7 layers, Band B = 8 layers, w = 64, eps = 1e-6,
+ * HS signal, z-score smoothing, R = min(128, K/4).  batch and budget are set
+ * to 1 and 4096.  Returns EPIKV_EINVAL_NULL if cfg is NULL. */
+int epikv_default_cfg(epikv_cfg* cfg);
+
+/* Static description of a status code (never NULL). */
+const char* epikv_strerror(int status);
+
+/* Validate a configuration without touching the device. */
+int epikv_check_cfg(const epikv_cfg* cfg);
+
+/*
+ * Scorer state carried from one call to the next (one flat device buffer,
+ * caller-owned; checkpoint = copy it, resume = copy it back).  Sections,
+ * each 256-byte aligned, at the offsets epikv_state_layout returns:
+ *   [0] int32 n_tok[B]            tokens the scorer has consumed per sequence
+ *   [1] float ring[B][n_sig][w-1] the last min(w-1, samples) signal samples,
+ *                                 right-aligned (slot w-2 newest), unused
+ *                                 slots 0
+ *   [2] bf16  h_prev[B][n_band][D] HS: hidden state of the last token
+ *   [3] float range[2][B][L][2][H][d] Lag-KV: per-channel min (first half)
+ *                                 and max of the previous chunk
+ * n_sig = n_band_a + n_band_b for HS, 1 for Lag-KV.  An HS stream yields a
+ * sample for every token but its first (which has no predecessor); a
+ * Lag-KV stream for every token.  Sections a signal does not use have size
+ * 0.  Returns the total size in bytes, or 0 for an invalid cfg.
+ */
+size_t epikv_state_bytes(const epikv_cfg* cfg);
+
+/* Byte offsets of the four state sections (host array of 4), see above.
+ * Returns EPIKV_OK or a host error code. */
+int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]);
+
+/* Device scratch that epikv_score and epikv_evict_step need for a chunk of
+ * `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
+size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
+
+/* Reset a state buffer of epikv_state_bytes(cfg) bytes to the start of a
+ * stream (every section zero).  Uses a fill kernel, so it may be captured
+ * in a HIP graph. */
+int epikv_state_init(const epikv_cfg* cfg, void* state, hipStream_t stream);
+
+/*
+ * epikv_score -- per-token signal of `chunk` new tokens of every sequence.
+ *
+ * HS signal (Sec. 3.2, Eq. 1): sig[l][b][c] = ||h_l(b,c) - h_l(b,c-1)||_2 for
+ * each band layer l, computed in fp32 from bf16 inputs.  h_l(b,-1) is
+ * state_in.h_prev; for a fresh stream (n_tok = 0) the first token has no
+ * sample and sig is 0 there.
+ *   hidden      host array of n_band device pointers (Band A first); the
+ *               row of token c of sequence b at layer l starts at
+ *               hidden[l] + b*ld_seq + c*ld_tok (bf16 elements); pointers
+ *               16-byte aligned, ld_tok and ld_seq multiples of 8, rows of
+ *               D elements.
+ *   pool, page_table, ld_pt, n_cached   unused (may be NULL / 0).
+ * Lag-KV signal (Sec. 3.3): the chunk's tokens are positions
+ * [n_cached[b] - chunk, n_cached[b]) of the paged cache (page_table
+ * int32 [B][ld_pt]).  Each channel of the token's key and value rows is
+ * normalised by the previous chunk's per-channel range from state_in
+ * (x - mn) / (mx - mn + eps) (the first chunk of a stream uses its own
+ * range), the population variance over the head dimension is taken for K
+ * and V and summed, and the sum is averaged over layers and KV heads:
+ * sig[0][b][c].  hidden may be NULL.  Needs
+ * epikv_workspace_bytes(cfg, chunk) bytes of workspace (ignored for HS).
+ *
+ * state_out receives h_prev (HS) or this chunk's range (Lag-KV); its
+ * counters and ring are written by epikv_zscore, so a step is complete only
+ * after both calls.  state_in and state_out must not overlap.
+ * sig: float [n_sig][B][chunk].
+ * Sequences whose positions fall outside [0, ld_pt*page_size) or whose pages
+ * are outside the pool get sig 0 for the affected tokens.
+ */
+int epikv_score(const epikv_cfg* cfg, int32_t chunk,
+                const void* const* hidden, int64_t ld_tok, int64_t ld_seq,
+                const epikv_pool* pool, const int32_t* page_table,
+                int64_t ld_pt, const int32_t* n_cached,
+                const void* state_in, void* state_out, float* sig,
+                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * epikv_zscore -- smoothing and band combination (Eq. 3 or Eq. 2, Fig. 1).
+ *
+ * For each signal row the new samples follow the w-1 carried in
+ * state_in.ring; each token's window is the last min(w, available) samples
+ * up to and including its own.  Z: (x - mu) / (sigma + eps) with the
+ * population sigma; MEAN: mu; RAW: x.  Tokens without a sample get 0.  The
+ * frozen score s = mean over Band A rows - mean over Band B rows (Lag-KV:
+ * the single row) is written to scores[b*ld_s + n_cached[b] - chunk + c].
+ * Sequences with n_cached < chunk or n_cached > ld_s are skipped.
+ *   sig       float [n_sig][B][chunk] from epikv_score.
+ *   smoothed  optional (may be NULL) float [n_sig][B][chunk]: per-row
+ *             smoothed values.
+ * state_out receives n_tok += chunk and the updated ring.
+ */
+int epikv_zscore(const epikv_cfg* cfg, int32_t chunk, const float* sig,
+                 const int32_t* n_cached, const void* state_in,
+                 void* state_out, float* scores, int64_t ld_s,
+                 float* smoothed, hipStream_t stream);
+
+/*
+ * epikv_select -- positions that survive (Sec. 3.1, Sec. 3.3, App. D).
+ *
+ * Per sequence with N = n_cached[b] and P = n_prefix[b]:
+ *   N <= K          keep all: keep_idx = 0..N-1, n_keep = N;
+ *   P + R >= K < N  seq_status BUDGET, n_keep = -1;
+ *   otherwise       keep [0, P), [N-R, N) and the K-P-R best positions of
+ *                   [P, N-R): higher score first, equal scores by lower
+ *                   position, -0 equal to +0, NaN below every number.
+ *                   n_keep = K.
+ * keep_idx is int32 [B][K], ascending.  scores float [B][ld_s].
+ * N < 0, N > ld_s, P < 0: seq_status RANGE, n_keep = -1.
+ */
+int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
+                 const int32_t* n_cached, const int32_t* n_prefix,
+                 int32_t* keep_idx, int32_t* n_keep, int32_t* seq_status,
+                 hipStream_t stream);
+
+/*
+ * epikv_compact -- order-preserving rebuild of the cache (App. H).
+ *
+ * For every sequence with n_keep[b] >= 0 and every j < n_keep[b]: the row
+ * of position keep_idx[b][j] (through src_pt, int32 [B][ld_src_pt]) is
+ * copied bit for bit to slot j (through dst_pt, int32 [B][ld_dst_pt]) for
+ * every layer, K and V.  Slots >= n_keep[b] are not written.  When
+ * src_scores/dst_scores (float [B][ld_s]) are given, dst_scores[b][j] =
+ * src_scores[b][keep_idx[b][j]]; likewise src_pos/dst_pos (int32 [B][ld_s]).
+ * Out of place: destination pages must not be source pages of any sequence
+ * (not checked), and dst_scores/dst_pos must not overlap their sources.
+ * Rows whose index or page id is out of range are skipped and set
+ * seq_status[b] = RANGE when seq_status is given.
+ */
+int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src,
+                  const int32_t* src_pt, int64_t ld_src_pt,
+                  const epikv_pool* dst, const int32_t* dst_pt,
+                  int64_t ld_dst_pt, const int32_t* keep_idx,
+                  const int32_t* n_keep, const float* src_scores,
+                  float* dst_scores, const int32_t* src_pos, int32_t* dst_pos,
+                  int64_t ld_s, int32_t* seq_status, hipStream_t stream);
+
+/* Arguments of one eviction step (host struct; pointers as above). */
+typedef struct epikv_step_io {
+  int32_t chunk;                /* new tokens per sequence (eviction cadence) */
+  const void* const* hidden;    /* HS: host array of n_band device pointers */
+  int64_t ld_tok, ld_seq;
+  const int32_t* n_cached;      /* [B] cached tokens incl. the new chunk */
+  const int32_t* n_prefix;      /* [B] prefill tokens, always kept */
+  epikv_pool src;               /* cache before the step */
+  const int32_t* src_pt;
+  int64_t ld_src_pt;
+  epikv_pool dst;               /* cache after the step (disjoint pages) */
+  const int32_t* dst_pt;
+  int64_t ld_dst_pt;
+  float* scores;                /* [B][ld_s] frozen scores; the chunk's are written */
+  float* dst_scores;            /* [B][ld_s] compacted scores (optional) */
+  const int32_t* src_pos;       /* [B][ld_s] optional token ids ... */
+  int32_t* dst_pos;             /* ... and their compacted copy */
+  int64_t ld_s;
+  const void* state_in;
+  void* state_out;
+  int32_t* keep_idx;            /* [B][K] */
+  int32_t* n_keep;              /* [B] */
+  int32_t* seq_status;          /* [B] */
+  void* workspace;
+  size_t workspace_bytes;       /* >= epikv_workspace_bytes(cfg, chunk) */
+} epikv_step_io;
+
+/*
+ * epikv_evict_step -- score, zscore, select and compact in one call, all on
+ * `stream`, with no host synchronisation.  Equivalent to the four calls
+ * above with the signal in the workspace; sequences with n_cached < chunk
+ * are flagged RANGE by the select stage.
+ */
+int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
+                     hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EPIKV_H */

@@ -1,0 +1,517 @@
+// C-ABI host layer: argument validation, state/workspace layout and kernel
+// launches.  Every host-detectable error is returned before anything is
+// enqueued; nothing here allocates, synchronises or keeps global state.
+#include <math.h>
+#include <string.h>
+
+#include "epikv_internal.h"
+
+#define EPIKV_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace epikv {
+
+size_t lagkv_lds_bytes(int C, int H, int d);
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int n_band(const epikv_cfg* c) { return c->n_band_a + c->n_band_b; }
+
+int n_sig(const epikv_cfg* c) { return c->signal == EPIKV_SIGNAL_HS ? n_band(c) : 1; }
+
+int recent_of(const epikv_cfg* c) {
+  return c->recent >= 0 ? c->recent : (c->budget / 4 < 128 ? c->budget / 4 : 128);
+}
+
+int row_bytes(const epikv_cfg* c) { return c->n_kv_heads * c->head_dim * 2; }
+
+int pages_for(int64_t tokens, int page_size) { return (int)((tokens + page_size - 1) / page_size); }
+
+struct Layout {
+  size_t off[4];
+  size_t size[4];
+  size_t total;
+};
+
+Layout state_layout(const epikv_cfg* c) {
+  Layout L;
+  const size_t B = (size_t)c->batch;
+  L.size[0] = 4 * B;
+  L.size[1] = 4 * B * (size_t)n_sig(c) * (size_t)(c->window - 1);
+  L.size[2] = c->signal == EPIKV_SIGNAL_HS ? 2 * B * (size_t)n_band(c) * (size_t)c->hidden : 0;
+  L.size[3] = c->signal == EPIKV_SIGNAL_LAGKV
+                  ? 4 * 2 * B * (size_t)c->n_layers * 2 * (size_t)c->n_kv_heads * (size_t)c->head_dim
+                  : 0;
+  size_t o = 0;
+  for (int i = 0; i < 4; ++i) {
+    L.off[i] = o;
+    o = align_up(o + L.size[i]);
+  }
+  L.total = o;
+  return L;
+}
+
+size_t sig_bytes(const epikv_cfg* c, int chunk) {
+  return align_up(4 * (size_t)n_sig(c) * (size_t)c->batch * (size_t)chunk);
+}
+
+size_t partial_bytes(const epikv_cfg* c, int chunk) {
+  if (c->signal != EPIKV_SIGNAL_LAGKV) return 0;
+  return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk);
+}
+
+int check_cfg(const epikv_cfg* c) {
+  if (!c) return EPIKV_EINVAL_NULL;
+  if (c->signal != EPIKV_SIGNAL_HS && c->signal != EPIKV_SIGNAL_LAGKV) return EPIKV_EINVAL_PARAM;
+  if (c->smoothing < EPIKV_SMOOTH_Z || c->smoothing > EPIKV_SMOOTH_RAW) return EPIKV_EINVAL_PARAM;
+  if (c->window < 1 || c->window > EPIKV_MAX_WINDOW) return EPIKV_EINVAL_PARAM;
+  if (!(c->eps >= 0.f) || !isfinite(c->eps)) return EPIKV_EINVAL_PARAM;
+  if (c->budget < 1) return EPIKV_EINVAL_PARAM;
+  if (c->recent < -1) return EPIKV_EINVAL_PARAM;
+  if (c->batch < 1 || c->batch > 65535) return EPIKV_EINVAL_SHAPE;
+  if (c->page_size < 1 || c->page_size > 1024) return EPIKV_EINVAL_SHAPE;
+  if (c->n_layers < 1 || c->n_layers > 1024) return EPIKV_EINVAL_SHAPE;
+  if (c->n_kv_heads < 1) return EPIKV_EINVAL_SHAPE;
+  if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256) return EPIKV_EINVAL_SHAPE;
+  const int hd = c->n_kv_heads * c->head_dim;
+  if (hd > 2048) return EPIKV_EINVAL_SHAPE;
+  const int row_vec = hd / 8;
+  // The compaction tile (one page of one plane) must fit the per-thread
+  // column budget of one workgroup.
+  if ((int64_t)c->page_size * row_vec > (int64_t)kCompactThreads * kCompactMaxVec) return EPIKV_EINVAL_SHAPE;
+  if (c->signal == EPIKV_SIGNAL_LAGKV && (kScoreThreads % row_vec) != 0) return EPIKV_EINVAL_SHAPE;
+  if (c->signal == EPIKV_SIGNAL_HS) {
+    if (c->n_band_a < 1 || c->n_band_b < 0 || n_band(c) > EPIKV_MAX_BAND) return EPIKV_EINVAL_SHAPE;
+    if (c->hidden < 8 || c->hidden > 16384 || (c->hidden % 8) != 0) return EPIKV_EINVAL_SHAPE;
+  }
+  return EPIKV_OK;
+}
+
+int check_pool(const epikv_pool* p) {
+  if (!p || !p->base) return EPIKV_EINVAL_NULL;
+  if (p->n_pages < 1 || p->n_pages > INT32_MAX) return EPIKV_EINVAL_SHAPE;
+  if (p->stride_layer < 0 || p->stride_kv < 0 || p->stride_page < 0) return EPIKV_EINVAL_SHAPE;
+  if (!aligned16(p->base) || (p->stride_layer % 16) || (p->stride_kv % 16) || (p->stride_page % 16))
+    return EPIKV_EALIGN;
+  return EPIKV_OK;
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+int launched(hipError_t e) { return e == hipSuccess ? EPIKV_OK : EPIKV_ELAUNCH; }
+
+// ---------------------------------------------------------------------------
+// Per-stage validation + argument building
+// ---------------------------------------------------------------------------
+int check_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,
+                int64_t ld_seq, const epikv_pool* pool, const int32_t* page_table, int64_t ld_pt,
+                const int32_t* n_cached, const void* state_in, void* state_out, float* sig,
+                void* ws, size_t ws_bytes, bool check_ws) {
+  int st = check_cfg(c);
+  if (st) return st;
+  if (!state_in || !state_out || !sig) return EPIKV_EINVAL_NULL;
+  if (chunk < 1) return EPIKV_EINVAL_SHAPE;
+  if (!aligned16(state_in) || !aligned16(state_out)) return EPIKV_EALIGN;
+  const size_t sb = state_layout(c).total;
+  if (overlap(state_in, sb, state_out, sb)) return EPIKV_EALIAS;
+  if (c->signal == EPIKV_SIGNAL_HS) {
+    if (!hidden) return EPIKV_EINVAL_NULL;
+    for (int l = 0; l < n_band(c); ++l) {
+      if (!hidden[l]) return EPIKV_EINVAL_NULL;
+      if (!aligned16(hidden[l])) return EPIKV_EALIGN;
+    }
+    if (ld_tok < 0 || ld_seq < 0) return EPIKV_EINVAL_SHAPE;
+    if (chunk > 1 && ld_tok < c->hidden) return EPIKV_EINVAL_SHAPE;
+    if ((ld_tok % 8) || (ld_seq % 8)) return EPIKV_EALIGN;
+  } else {
+    st = check_pool(pool);
+    if (st) return st;
+    if (!page_table || !n_cached) return EPIKV_EINVAL_NULL;
+    if (ld_pt < 1) return EPIKV_EINVAL_SHAPE;
+    if (lagkv_lds_bytes(chunk, c->n_kv_heads, c->head_dim) > (size_t)kLagMaxLds) return EPIKV_EINVAL_SHAPE;
+    if (check_ws) {
+      if (!ws || ws_bytes < sig_bytes(c, chunk) + partial_bytes(c, chunk)) return EPIKV_EWORKSPACE;
+      if (!aligned16(ws)) return EPIKV_EALIGN;
+    }
+  }
+  return EPIKV_OK;
+}
+
+ScoreHsArgs hs_args(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,
+                    int64_t ld_seq, const void* state_in, void* state_out, float* sig) {
+  const Layout L = state_layout(c);
+  ScoreHsArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int l = 0; l < n_band(c); ++l) a.hidden[l] = (const uint16_t*)hidden[l];
+  a.ld_tok = ld_tok;
+  a.ld_seq = ld_seq;
+  a.B = c->batch;
+  a.C = chunk;
+  a.D = c->hidden;
+  a.n_band = n_band(c);
+  a.seg_len = kScoreSeg;
+  a.n_tok_in = (const int32_t*)state_in;
+  a.h_prev_in = (const uint16_t*)((const char*)state_in + L.off[2]);
+  a.h_prev_out = (uint16_t*)((char*)state_out + L.off[2]);
+  a.sig = sig;
+  return a;
+}
+
+void lag_args(const epikv_cfg* c, int32_t chunk, const epikv_pool* pool, const int32_t* pt,
+              int64_t ld_pt, const int32_t* n_cached, const void* state_in, void* state_out,
+              float* sig, float* partial, ScoreLagArgs* a, LagReduceArgs* r) {
+  const Layout L = state_layout(c);
+  a->base = (const char*)pool->base;
+  a->s_layer = pool->stride_layer;
+  a->s_kv = pool->stride_kv;
+  a->s_page = pool->stride_page;
+  a->n_pages = pool->n_pages;
+  a->pt = pt;
+  a->ld_pt = ld_pt;
+  a->n_cached = n_cached;
+  a->B = c->batch;
+  a->C = chunk;
+  a->L = c->n_layers;
+  a->H = c->n_kv_heads;
+  a->d = c->head_dim;
+  a->page_size = c->page_size;
+  a->eps = c->eps;
+  a->n_tok_in = (const int32_t*)state_in;
+  a->range_in = (const float*)((const char*)state_in + L.off[3]);
+  a->range_out = (float*)((char*)state_out + L.off[3]);
+  a->partial = partial;
+  r->partial = partial;
+  r->sig = sig;
+  r->B = c->batch;
+  r->C = chunk;
+  r->n_lk = 2 * c->n_layers;
+  r->inv_count = 1.0f / (float)(c->n_layers * c->n_kv_heads);
+}
+
+int run_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,
+              int64_t ld_seq, const epikv_pool* pool, const int32_t* pt, int64_t ld_pt,
+              const int32_t* n_cached, const void* state_in, void* state_out, float* sig,
+              float* partial, hipStream_t s) {
+  if (c->signal == EPIKV_SIGNAL_HS)
+    return launched(launch_score_hs(hs_args(c, chunk, hidden, ld_tok, ld_seq, state_in, state_out, sig), s));
+  ScoreLagArgs a;
+  LagReduceArgs r;
+  lag_args(c, chunk, pool, pt, ld_pt, n_cached, state_in, state_out, sig, partial, &a, &r);
+  return launched(launch_score_lagkv(a, r, s));
+}
+
+int check_zscore(const epikv_cfg* c, int32_t chunk, const float* sig, const int32_t* n_cached,
+                 const void* state_in, void* state_out, float* scores, int64_t ld_s) {
+  int st = check_cfg(c);
+  if (st) return st;
+  if (!sig || !n_cached || !state_in || !state_out || !scores) return EPIKV_EINVAL_NULL;
+  if (chunk < 1) return EPIKV_EINVAL_SHAPE;
+  if (ld_s < chunk) return EPIKV_EINVAL_SHAPE;
+  if (!aligned16(state_in) || !aligned16(state_out)) return EPIKV_EALIGN;
+  const size_t sb = state_layout(c).total;
+  if (overlap(state_in, sb, state_out, sb)) return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
+ZscoreArgs zscore_args(const epikv_cfg* c, int32_t chunk, const float* sig, const int32_t* n_cached,
+                       const void* state_in, void* state_out, float* scores, int64_t ld_s,
+                       float* smoothed) {
+  const Layout L = state_layout(c);
+  ZscoreArgs a;
+  a.sig = sig;
+  a.B = c->batch;
+  a.C = chunk;
+  a.n_sig = n_sig(c);
+  a.n_a = c->signal == EPIKV_SIGNAL_HS ? c->n_band_a : 1;
+  a.n_b = c->signal == EPIKV_SIGNAL_HS ? c->n_band_b : 0;
+  a.w = c->window;
+  a.mode = c->smoothing;
+  a.hs = c->signal == EPIKV_SIGNAL_HS ? 1 : 0;
+  a.eps = c->eps;
+  a.n_cached = n_cached;
+  a.n_tok_in = (const int32_t*)state_in;
+  a.ring_in = (const float*)((const char*)state_in + L.off[1]);
+  a.n_tok_out = (int32_t*)state_out;
+  a.ring_out = (float*)((char*)state_out + L.off[1]);
+  a.scores = scores;
+  a.ld_s = ld_s;
+  a.smoothed = smoothed;
+  return a;
+}
+
+int check_select(const epikv_cfg* c, const float* scores, int64_t ld_s, const int32_t* n_cached,
+                 const int32_t* n_prefix, int32_t* keep_idx, int32_t* n_keep, int32_t* seq_status) {
+  int st = check_cfg(c);
+  if (st) return st;
+  if (!scores || !n_cached || !n_prefix || !keep_idx || !n_keep || !seq_status) return EPIKV_EINVAL_NULL;
+  if (ld_s < 1 || ld_s > INT32_MAX) return EPIKV_EINVAL_SHAPE;
+  return EPIKV_OK;
+}
+
+SelectArgs select_args(const epikv_cfg* c, const float* scores, int64_t ld_s, const int32_t* n_cached,
+                       const int32_t* n_prefix, int32_t* keep_idx, int32_t* n_keep,
+                       int32_t* seq_status, int min_n) {
+  SelectArgs a;
+  a.scores = scores;
+  a.ld_s = ld_s;
+  a.n_cached = n_cached;
+  a.n_prefix = n_prefix;
+  a.B = c->batch;
+  a.K = c->budget;
+  a.R = recent_of(c);
+  a.min_n = min_n;
+  a.keep_idx = keep_idx;
+  a.n_keep = n_keep;
+  a.seq_status = seq_status;
+  return a;
+}
+
+int check_compact(const epikv_cfg* c, const epikv_pool* src, const int32_t* src_pt, int64_t ld_src_pt,
+                  const epikv_pool* dst, const int32_t* dst_pt, int64_t ld_dst_pt,
+                  const int32_t* keep_idx, const int32_t* n_keep, const float* src_scores,
+                  float* dst_scores, const int32_t* src_pos, int32_t* dst_pos, int64_t ld_s) {
+  int st = check_cfg(c);
+  if (st) return st;
+  st = check_pool(src);
+  if (st) return st;
+  st = check_pool(dst);
+  if (st) return st;
+  if (!src_pt || !dst_pt || !keep_idx || !n_keep) return EPIKV_EINVAL_NULL;
+  if ((src_scores == nullptr) != (dst_scores == nullptr)) return EPIKV_EINVAL_NULL;
+  if ((src_pos == nullptr) != (dst_pos == nullptr)) return EPIKV_EINVAL_NULL;
+  if (ld_src_pt < 1 || ld_dst_pt < pages_for(c->budget, c->page_size)) return EPIKV_EINVAL_SHAPE;
+  if ((dst_scores || dst_pos) && ld_s < 1) return EPIKV_EINVAL_SHAPE;
+  const size_t bytes = 4 * (size_t)c->batch * (size_t)(ld_s > 0 ? ld_s : 0);
+  if (dst_scores && overlap(src_scores, bytes, dst_scores, bytes)) return EPIKV_EALIAS;
+  if (dst_pos && overlap(src_pos, bytes, dst_pos, bytes)) return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
+CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_t* src_pt,
+                         int64_t ld_src_pt, const epikv_pool* dst, const int32_t* dst_pt,
+                         int64_t ld_dst_pt, const int32_t* keep_idx, const int32_t* n_keep,
+                         const float* src_scores, float* dst_scores, const int32_t* src_pos,
+                         int32_t* dst_pos, int64_t ld_s, int32_t* seq_status) {
+  CompactArgs a;
+  a.src = (const char*)src->base;
+  a.s_layer = src->stride_layer;
+  a.s_kv = src->stride_kv;
+  a.s_page = src->stride_page;
+  a.s_npages = src->n_pages;
+  a.dst = (char*)dst->base;
+  a.d_layer = dst->stride_layer;
+  a.d_kv = dst->stride_kv;
+  a.d_page = dst->stride_page;
+  a.d_npages = dst->n_pages;
+  a.src_pt = src_pt;
+  a.ld_src_pt = ld_src_pt;
+  a.dst_pt = dst_pt;
+  a.ld_dst_pt = ld_dst_pt;
+  a.keep_idx = keep_idx;
+  a.n_keep = n_keep;
+  a.src_scores = src_scores;
+  a.dst_scores = dst_scores;
+  a.src_pos = src_pos;
+  a.dst_pos = dst_pos;
+  a.ld_s = ld_s;
+  a.seq_status = seq_status;
+  a.B = c->batch;
+  a.K = c->budget;
+  a.page_size = c->page_size;
+  a.row_bytes = row_bytes(c);
+  a.n_lk = 2 * c->n_layers;
+  a.lk_per_block = 8;
+  a.pages_per_seq = pages_for(c->budget, c->page_size);
+  return a;
+}
+
+__global__ void k_fill(FillArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k = i; k < a.n_words; k += stride) a.p[k] = a.value;
+}
+
+}  // namespace
+
+hipError_t launch_fill(const FillArgs& a, hipStream_t s) {
+  int64_t blocks = (a.n_words + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_fill, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace epikv
+
+using namespace epikv;
+
+// ---------------------------------------------------------------------------
+// Exported entry points
+// ---------------------------------------------------------------------------
+EPIKV_EXPORT int epikv_default_cfg(epikv_cfg* cfg) {
+  if (!cfg) return EPIKV_EINVAL_NULL;
+  cfg->batch = 1;
+  cfg->hidden = 4096;
+  cfg->n_layers = 32;
+  cfg->n_kv_heads = 8;
+  cfg->head_dim = 128;
+  cfg->page_size = 16;
+  cfg->n_band_a = 7;
+  cfg->n_band_b = 8;
+  cfg->window = 64;
+  cfg->eps = 1e-6f;
+  cfg->signal = EPIKV_SIGNAL_HS;
+  cfg->smoothing = EPIKV_SMOOTH_Z;
+  cfg->budget = 4096;
+  cfg->recent = -1;
+  return EPIKV_OK;
+}
+
+EPIKV_EXPORT const char* epikv_strerror(int status) {
+  switch (status) {
+    case EPIKV_OK: return "ok";
+    case EPIKV_EINVAL_NULL: return "a required pointer is NULL";
+    case EPIKV_EINVAL_SHAPE: return "a size is outside the supported range";
+    case EPIKV_EINVAL_PARAM: return "invalid parameter (budget, window, eps or enum)";
+    case EPIKV_EALIGN: return "pointer, stride or leading dimension misaligned";
+    case EPIKV_EWORKSPACE: return "workspace missing or too small";
+    case EPIKV_EALIAS: return "an output overlaps an input it must not overlap";
+    case EPIKV_ELAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+EPIKV_EXPORT int epikv_check_cfg(const epikv_cfg* cfg) { return check_cfg(cfg); }
+
+EPIKV_EXPORT size_t epikv_state_bytes(const epikv_cfg* cfg) {
+  if (check_cfg(cfg)) return 0;
+  return state_layout(cfg).total;
+}
+
+EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]) {
+  const int st = check_cfg(cfg);
+  if (st) return st;
+  if (!offsets) return EPIKV_EINVAL_NULL;
+  const Layout L = state_layout(cfg);
+  for (int i = 0; i < 4; ++i) offsets[i] = L.off[i];
+  return EPIKV_OK;
+}
+
+EPIKV_EXPORT size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk) {
+  if (check_cfg(cfg) || chunk < 1) return 0;
+  return sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk);
+}
+
+EPIKV_EXPORT int epikv_state_init(const epikv_cfg* cfg, void* state, hipStream_t stream) {
+  const int st = check_cfg(cfg);
+  if (st) return st;
+  if (!state) return EPIKV_EINVAL_NULL;
+  if (!aligned16(state)) return EPIKV_EALIGN;
+  FillArgs f;
+  f.p = (uint32_t*)state;
+  f.n_words = (int64_t)(state_layout(cfg).total / 4);
+  f.value = 0u;
+  return launched(launch_fill(f, stream));
+}
+
+EPIKV_EXPORT int epikv_score(const epikv_cfg* cfg, int32_t chunk, const void* const* hidden,
+                             int64_t ld_tok, int64_t ld_seq, const epikv_pool* pool,
+                             const int32_t* page_table, int64_t ld_pt, const int32_t* n_cached,
+                             const void* state_in, void* state_out, float* sig, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  const int st = check_score(cfg, chunk, hidden, ld_tok, ld_seq, pool, page_table, ld_pt, n_cached,
+                             state_in, state_out, sig, workspace, workspace_bytes, true);
+  if (st) return st;
+  // Standalone: the Lag-KV partial sums use the start of the workspace.
+  return run_score(cfg, chunk, hidden, ld_tok, ld_seq, pool, page_table, ld_pt, n_cached, state_in,
+                   state_out, sig, (float*)workspace, stream);
+}
+
+EPIKV_EXPORT int epikv_zscore(const epikv_cfg* cfg, int32_t chunk, const float* sig,
+                              const int32_t* n_cached, const void* state_in, void* state_out,
+                              float* scores, int64_t ld_s, float* smoothed, hipStream_t stream) {
+  const int st = check_zscore(cfg, chunk, sig, n_cached, state_in, state_out, scores, ld_s);
+  if (st) return st;
+  return launched(launch_zscore(
+      zscore_args(cfg, chunk, sig, n_cached, state_in, state_out, scores, ld_s, smoothed), stream));
+}
+
+EPIKV_EXPORT int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
+                              const int32_t* n_cached, const int32_t* n_prefix, int32_t* keep_idx,
+                              int32_t* n_keep, int32_t* seq_status, hipStream_t stream) {
+  const int st = check_select(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status);
+  if (st) return st;
+  return launched(launch_select(
+      select_args(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status, 0), stream));
+}
+
+EPIKV_EXPORT int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src, const int32_t* src_pt,
+                               int64_t ld_src_pt, const epikv_pool* dst, const int32_t* dst_pt,
+                               int64_t ld_dst_pt, const int32_t* keep_idx, const int32_t* n_keep,
+                               const float* src_scores, float* dst_scores, const int32_t* src_pos,
+                               int32_t* dst_pos, int64_t ld_s, int32_t* seq_status,
+                               hipStream_t stream) {
+  const int st = check_compact(cfg, src, src_pt, ld_src_pt, dst, dst_pt, ld_dst_pt, keep_idx, n_keep,
+                               src_scores, dst_scores, src_pos, dst_pos, ld_s);
+  if (st) return st;
+  return launched(launch_compact(compact_args(cfg, src, src_pt, ld_src_pt, dst, dst_pt, ld_dst_pt,
+                                              keep_idx, n_keep, src_scores, dst_scores, src_pos,
+                                              dst_pos, ld_s, seq_status),
+                                 stream));
+}
+
+EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io, hipStream_t stream) {
+  if (!io) return EPIKV_EINVAL_NULL;
+  int st = check_cfg(cfg);
+  if (st) return st;
+  if (io->chunk < 1) return EPIKV_EINVAL_SHAPE;
+  if (!io->workspace || io->workspace_bytes < epikv_workspace_bytes(cfg, io->chunk))
+    return EPIKV_EWORKSPACE;
+  if (!aligned16(io->workspace)) return EPIKV_EALIGN;
+  st = check_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
+                   io->ld_src_pt, io->n_cached, io->state_in, io->state_out,
+                   (float*)io->workspace, io->workspace, io->workspace_bytes, false);
+  if (st) return st;
+  st = check_zscore(cfg, io->chunk, (const float*)io->workspace, io->n_cached, io->state_in,
+                    io->state_out, io->scores, io->ld_s);
+  if (st) return st;
+  st = check_select(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix, io->keep_idx, io->n_keep,
+                    io->seq_status);
+  if (st) return st;
+  st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
+                     io->keep_idx, io->n_keep, io->scores, io->dst_scores, io->src_pos, io->dst_pos,
+                     io->ld_s);
+  if (st) return st;
+  const size_t ws_state = state_layout(cfg).total;
+  if (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
+      overlap(io->workspace, io->workspace_bytes, io->state_out, ws_state))
+    return EPIKV_EALIAS;
+
+  float* sig = (float*)io->workspace;
+  float* partial = (float*)((char*)io->workspace + sig_bytes(cfg, io->chunk));
+  st = run_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
+                 io->ld_src_pt, io->n_cached, io->state_in, io->state_out, sig, partial, stream);
+  if (st) return st;
+  st = launched(launch_zscore(zscore_args(cfg, io->chunk, sig, io->n_cached, io->state_in,
+                                          io->state_out, io->scores, io->ld_s, nullptr),
+                              stream));
+  if (st) return st;
+  st = launched(launch_select(select_args(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix,
+                                          io->keep_idx, io->n_keep, io->seq_status, io->chunk),
+                              stream));
+  if (st) return st;
+  const bool with_scores = io->dst_scores != nullptr;
+  return launched(launch_compact(
+      compact_args(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
+                   io->keep_idx, io->n_keep, with_scores ? io->scores : nullptr, io->dst_scores,
+                   io->src_pos, io->dst_pos, io->ld_s, io->seq_status),
+      stream));
+}

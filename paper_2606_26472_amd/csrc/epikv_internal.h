@@ -1,0 +1,138 @@
+// Internal interface between the C-ABI host layer (epikv_api.hip) and the
+// gfx950 kernels.  Each kernel takes one argument struct by value.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "epikv.h"
+
+namespace epikv {
+
+// 16-byte vector used for every global load/store of bf16 rows.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ u32x4 ld_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void st_stream(void* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+// Sum over the 64 lanes of a wavefront with a fixed butterfly order, so the
+// result is identical on every lane and from run to run.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Argument structs
+// ---------------------------------------------------------------------------
+struct ScoreHsArgs {
+  const uint16_t* hidden[EPIKV_MAX_BAND];  // per band layer, Band A first
+  int64_t ld_tok, ld_seq;                  // bf16 elements
+  int32_t B, C, D, n_band, seg_len;
+  const int32_t* n_tok_in;                 // state [B]
+  const uint16_t* h_prev_in;               // state [B][n_band][D]
+  uint16_t* h_prev_out;
+  float* sig;                              // [n_band][B][C]
+};
+
+struct ScoreLagArgs {
+  const char* base;                        // pool
+  int64_t s_layer, s_kv, s_page, n_pages;
+  const int32_t* pt;
+  int64_t ld_pt;
+  const int32_t* n_cached;
+  int32_t B, C, L, H, d, page_size;
+  float eps;
+  const int32_t* n_tok_in;
+  const float* range_in;                   // [2][B][L][2][H][d]
+  float* range_out;
+  float* partial;                          // [B][2L][C]
+};
+
+struct LagReduceArgs {
+  const float* partial;                    // [B][2L][C]
+  float* sig;                              // [B][C]
+  int32_t B, C, n_lk;
+  float inv_count;                         // 1 / (L*H)
+};
+
+struct ZscoreArgs {
+  const float* sig;                        // [n_sig][B][C]
+  int32_t B, C, n_sig, n_a, n_b, w, mode, hs;
+  float eps;
+  const int32_t* n_cached;
+  const int32_t* n_tok_in;
+  const float* ring_in;                    // [B][n_sig][w-1]
+  int32_t* n_tok_out;
+  float* ring_out;
+  float* scores;
+  int64_t ld_s;
+  float* smoothed;                         // optional [n_sig][B][C]
+};
+
+struct SelectArgs {
+  const float* scores;
+  int64_t ld_s;
+  const int32_t* n_cached;
+  const int32_t* n_prefix;
+  int32_t B, K, R, min_n;
+  int32_t* keep_idx;                       // [B][K]
+  int32_t* n_keep;
+  int32_t* seq_status;
+};
+
+struct CompactArgs {
+  const char* src;
+  int64_t s_layer, s_kv, s_page, s_npages;
+  char* dst;
+  int64_t d_layer, d_kv, d_page, d_npages;
+  const int32_t* src_pt;
+  int64_t ld_src_pt;
+  const int32_t* dst_pt;
+  int64_t ld_dst_pt;
+  const int32_t* keep_idx;                 // [B][K]
+  const int32_t* n_keep;
+  const float* src_scores;
+  float* dst_scores;
+  const int32_t* src_pos;
+  int32_t* dst_pos;
+  int64_t ld_s;
+  int32_t* seq_status;                     // optional
+  int32_t B, K, page_size, row_bytes, n_lk, lk_per_block, pages_per_seq;
+};
+
+struct FillArgs {
+  uint32_t* p;
+  int64_t n_words;
+  uint32_t value;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (return the HIP error of the launch; never synchronise)
+// ---------------------------------------------------------------------------
+hipError_t launch_score_hs(const ScoreHsArgs& a, hipStream_t s);
+hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r,
+                              hipStream_t s);
+hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
+hipError_t launch_fill(const FillArgs& a, hipStream_t s);
+
+// Tunables the host layer validates against.
+constexpr int kScoreThreads = 256;
+constexpr int kScoreSeg = 32;            // tokens per score_hs workgroup
+constexpr int kZscoreTile = 256;         // tokens per zscore workgroup
+constexpr int kSelectThreads = 1024;
+constexpr int kCompactThreads = 256;
+constexpr int kCompactMaxVec = 16;       // 16-byte vectors per thread per (layer, K|V)
+constexpr int kLagMaxLds = 48 * 1024;
+
+}  // namespace epikv

@@ -1,0 +1,211 @@
+// Lag-normalised key+value variance, Sec. 3.3 (Lag-KV):
+//   x~ = (x - mn) / (mx - mn + eps)   per channel, with (mn, mx) the range
+//        of the previous chunk at the same (layer, K|V, head, channel);
+//   v(t, l, kv, h) = population variance of x~ over the head dimension;
+//   q(t) = mean over (layer, head) of v(t, l, K, h) + v(t, l, V, h).
+// The chunk's own per-channel range is written out as the next chunk's
+// reference.  The first chunk of a stream, with no previous chunk, is
+// normalised by its own range.
+//
+// Kernel 1: one 256-thread workgroup per (layer, K|V) plane and sequence
+// streams the chunk's rows of that plane from the paged pool.  Thread i owns
+// 8 channels (one 16-byte column) of a row; the d/8 lanes of one head reduce
+// the variance with butterfly shuffles (two passes: mean, then squared
+// deviations), and per-(token, head) variances go to LDS.  The workgroup
+// then writes per-token sums over its heads to partial[b][plane][c].
+// Kernel 2 sums the 2L planes in a fixed order and divides by L*H.
+#include "epikv_internal.h"
+
+namespace epikv {
+namespace {
+
+__device__ __forceinline__ float group_sum(float v, int width) {
+  for (int off = width >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ void unpack8(u32x4 w, float x[8]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    x[2 * k] = bf16_lo(w[k]);
+    x[2 * k + 1] = bf16_hi(w[k]);
+  }
+}
+
+__global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
+  extern __shared__ float lds[];
+  const int tid = threadIdx.x;
+  const int lk = blockIdx.x;
+  const int b = blockIdx.y;
+  const int layer = lk >> 1;
+  const int kv = lk & 1;
+  const int HD = a.H * a.d;
+  const int row_vec = HD >> 3;                 // 16-byte columns per row
+  const int rpp = kScoreThreads / row_vec;     // rows per pass
+  const int col = tid % row_vec;
+  const int ro = tid / row_vec;
+  const int gl = a.d >> 3;                     // lanes per head
+  const int head = col / gl;
+  const int row_bytes = HD * 2;
+
+  float* vbuf = lds;                           // [C][H]
+  float* cmb = lds + a.C * a.H;                // [2][rpp][HD] range combine
+
+  const int N = a.n_cached[b];
+  const int start = N - a.C;
+  const bool seq_ok = start >= 0 && (int64_t)((N - 1) / a.page_size) < a.ld_pt;
+  const char* plane = a.base + (int64_t)layer * a.s_layer + (int64_t)kv * a.s_kv;
+  const int32_t* pt = a.pt + (int64_t)b * a.ld_pt;
+  const int64_t half = (int64_t)a.B * a.L * 2 * HD;
+  const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
+  const bool fresh = a.n_tok_in[b] <= 0;
+
+  // Address of this thread's column of chunk row r, or nullptr.
+  auto row_ptr = [&](int r) -> const char* {
+    if (!seq_ok) return nullptr;
+    const int pos = start + r;
+    const int pg = pt[pos / a.page_size];
+    if (pg < 0 || pg >= a.n_pages) return nullptr;
+    return plane + (int64_t)pg * a.s_page + (int64_t)(pos % a.page_size) * row_bytes + col * 16;
+  };
+
+  float mn[8], mx[8], cmn[8], cmx[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    cmn[e] = __builtin_huge_valf();
+    cmx[e] = -__builtin_huge_valf();
+  }
+
+  // Combine the per-thread ranges of the rpp threads sharing a column.
+  auto combine = [&]() {
+    if (ro < rpp) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cmb[ro * HD + col * 8 + e] = cmn[e];
+        cmb[(rpp + ro) * HD + col * 8 + e] = cmx[e];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float lo = cmb[col * 8 + e], hi = cmb[rpp * HD + col * 8 + e];
+      for (int q = 1; q < rpp; ++q) {
+        lo = fminf(lo, cmb[q * HD + col * 8 + e]);
+        hi = fmaxf(hi, cmb[(rpp + q) * HD + col * 8 + e]);
+      }
+      cmn[e] = lo;
+      cmx[e] = hi;
+    }
+    __syncthreads();
+  };
+
+  if (fresh) {
+    for (int r = ro; r < a.C && ro < rpp; r += rpp) {
+      const char* p = row_ptr(r);
+      if (!p) continue;
+      float x[8];
+      unpack8(ld_stream(p), x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cmn[e] = fminf(cmn[e], x[e]);
+        cmx[e] = fmaxf(cmx[e], x[e]);
+      }
+    }
+    combine();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = cmn[e];
+      mx[e] = cmx[e];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = a.range_in[rbase + e];
+      mx[e] = a.range_in[half + rbase + e];
+    }
+  }
+  float den[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) den[e] = mx[e] - mn[e] + a.eps;
+
+  const float inv_d = 1.0f / (float)a.d;
+  // All threads run the same trip count so that the head-group shuffles see
+  // every lane of the group.
+  const int trips = (a.C + rpp - 1) / rpp;
+  for (int it = 0; it < trips; ++it) {
+    const int r = it * rpp + ro;
+    const bool live = ro < rpp && r < a.C;
+    const char* p = live ? row_ptr(r) : nullptr;
+    float x[8];
+    if (p) {
+      unpack8(ld_stream(p), x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cmn[e] = fminf(cmn[e], x[e]);
+        cmx[e] = fmaxf(cmx[e], x[e]);
+        x[e] = (x[e] - mn[e]) / den[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.f;
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += x[e];
+    const float mu = group_sum(s, gl) * inv_d;
+    float q = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float dlt = x[e] - mu;
+      q = fmaf(dlt, dlt, q);
+    }
+    const float var = group_sum(q, gl) * inv_d;
+    if (live && (col % gl) == 0) vbuf[r * a.H + head] = p ? var : 0.f;
+  }
+  __syncthreads();
+  combine();
+
+  if (ro == 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a.range_out[rbase + e] = cmn[e];
+      a.range_out[half + rbase + e] = cmx[e];
+    }
+  }
+  float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
+  for (int r = tid; r < a.C; r += kScoreThreads) {
+    float s = 0.f;
+    for (int h = 0; h < a.H; ++h) s += vbuf[r * a.H + h];
+    part[r] = s;
+  }
+}
+
+__global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
+  const int c = blockIdx.x * kScoreThreads + threadIdx.x;
+  const int b = blockIdx.y;
+  if (c >= a.C) return;
+  const float* p = a.partial + (int64_t)b * a.n_lk * a.C + c;
+  float s = 0.f;
+  for (int lk = 0; lk < a.n_lk; ++lk) s += p[(int64_t)lk * a.C];
+  a.sig[(int64_t)b * a.C + c] = s * a.inv_count;
+}
+
+}  // namespace
+
+size_t lagkv_lds_bytes(int C, int H, int d) {
+  const int HD = H * d;
+  const int rpp = kScoreThreads / (HD / 8);
+  return (size_t)C * H * 4 + (size_t)2 * rpp * HD * 4;
+}
+
+hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
+  const size_t lds = lagkv_lds_bytes(a.C, a.H, a.d);
+  hipLaunchKernelGGL(k_score_lagkv, dim3(2 * a.L, a.B), dim3(kScoreThreads), lds, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_lag_reduce, dim3((r.C + kScoreThreads - 1) / kScoreThreads, r.B),
+                     dim3(kScoreThreads), 0, s, r);
+  return hipGetLastError();
+}
+
+}  // namespace epikv

@@ -1,0 +1,190 @@
+// Which positions survive an eviction step (Sec. 3.1, Sec. 3.3, App. D):
+// the prefill [0, P), the recency window [N-R, N) and the M = K-P-R best
+// positions of [P, N-R), exactly K in ascending order.
+//
+// Ranking key: the fp32 score mapped to an unsigned integer whose order is
+// the ranking (higher score = larger key), with -0 folded onto +0 and every
+// NaN mapped to 0, below -inf.  Equal keys rank by lower position.
+//
+// One 1024-thread workgroup per sequence:
+//   1. radix select of the M-th largest key over 11/11/10-bit digits: each
+//      pass histograms the keys that match the digits chosen so far (LDS
+//      atomics), a block-wide suffix scan finds the digit holding the M-th
+//      key.  After three passes the threshold T is exact and `need` says
+//      how many keys equal to T are kept;
+//   2. one ordered sweep over the positions in tiles of 1024: a ballot
+//      prefix count ranks the keys equal to T by position (the first `need`
+//      of them are kept) and a second one gives every kept position its
+//      output slot, so keep_idx comes out ascending without a sort.
+// Scores are re-read from global memory in each pass (they stay in L2),
+// so N is not limited by LDS.
+#include "epikv_internal.h"
+
+namespace epikv {
+namespace {
+
+constexpr int kWaves = kSelectThreads / 64;
+
+__device__ __forceinline__ uint32_t rank_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;  // NaN: lowest
+  if (u == 0x80000000u) u = 0u;                     // -0 == +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Inclusive scan over the workgroup in thread order.
+__device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t v, uint32_t* wsum) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  if (lane == 63) wsum[wave] = v;
+  __syncthreads();
+  uint32_t add = 0;
+  for (int w = 0; w < wave; ++w) add += wsum[w];
+  __syncthreads();
+  return v + add;
+}
+
+// Exclusive rank of this lane's flag among the workgroup's set flags, and
+// the workgroup total.
+__device__ __forceinline__ uint32_t block_flag_rank(bool flag, uint32_t* wsum, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const uint64_t m = __ballot(flag);
+  const uint32_t below = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+  if (lane == 0) wsum[wave] = (uint32_t)__popcll(m);
+  __syncthreads();
+  uint32_t pre = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t x = wsum[w];
+    pre += (w < wave) ? x : 0u;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + below;
+}
+
+__global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
+  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t wsum[kWaves];
+  __shared__ uint32_t sel_digit, sel_above;
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int N = a.n_cached[b];
+  const int P = a.n_prefix[b];
+  const int K = a.K;
+  const int R = a.R;
+  int32_t* out = a.keep_idx + (int64_t)b * K;
+
+  if (N < a.min_n || (int64_t)N > a.ld_s || P < 0) {
+    if (tid == 0) {
+      a.n_keep[b] = -1;
+      a.seq_status[b] = EPIKV_SEQ_RANGE;
+    }
+    return;
+  }
+  if (N <= K) {
+    for (int j = tid; j < N; j += kSelectThreads) out[j] = j;
+    if (tid == 0) {
+      a.n_keep[b] = N;
+      a.seq_status[b] = EPIKV_SEQ_OK;
+    }
+    return;
+  }
+  if ((int64_t)P + R >= K) {
+    if (tid == 0) {
+      a.n_keep[b] = -1;
+      a.seq_status[b] = EPIKV_SEQ_BUDGET;
+    }
+    return;
+  }
+
+  const float* s = a.scores + (int64_t)b * a.ld_s;
+  const int lo = P, hi = N - R;  // eligible positions [lo, hi)
+  uint32_t prefix = 0u, mask = 0u;
+  uint32_t k = (uint32_t)(K - P - R);  // rank (1-based) of the threshold key
+
+  const int shifts[3] = {21, 10, 0};
+  const int nbits[3] = {11, 11, 10};
+#pragma unroll 1
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = shifts[pass];
+    const int nb = 1 << nbits[pass];
+    const uint32_t dmask = (uint32_t)nb - 1u;
+    for (int i = tid; i < nb; i += kSelectThreads) hist[i] = 0u;
+    __syncthreads();
+    for (int i = lo + tid; i < hi; i += kSelectThreads) {
+      const uint32_t key = rank_key(s[i]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
+    }
+    __syncthreads();
+    // Thread t owns the bpt bins just below nb - t*bpt (descending order),
+    // so the inclusive scan counts keys whose digit is >= its lowest bin.
+    const int bpt = nb / kSelectThreads;
+    const int top = nb - 1 - tid * bpt;
+    uint32_t local = 0u;
+    for (int q = 0; q < bpt; ++q) local += hist[top - q];
+    const uint32_t incl = block_inclusive_scan(local, wsum);
+    const uint32_t excl = incl - local;
+    if (excl < k && k <= incl) {
+      uint32_t above = excl;
+      int d = top - bpt + 1;
+      for (int q = 0; q < bpt; ++q) {
+        const uint32_t h = hist[top - q];
+        if (above + h >= k) {
+          d = top - q;
+          break;
+        }
+        above += h;
+      }
+      sel_digit = (uint32_t)d;
+      sel_above = above;
+    }
+    __syncthreads();
+    prefix |= sel_digit << shift;
+    mask |= dmask << shift;
+    k -= sel_above;
+    __syncthreads();
+  }
+
+  const uint32_t T = prefix;
+  const uint32_t need = k;  // keys equal to T that are kept, lowest positions first
+  uint32_t eq_seen = 0u, written = 0u;
+  for (int t0 = 0; t0 < N; t0 += kSelectThreads) {
+    const int i = t0 + tid;
+    const bool valid = i < N;
+    const bool prot = valid && (i < lo || i >= hi);
+    const bool elig = valid && !prot;
+    const uint32_t key = elig ? rank_key(s[i]) : 0u;
+    const bool gt = elig && key > T;
+    const bool eq = elig && key == T;
+    uint32_t eq_tot;
+    const uint32_t eq_rank = eq_seen + block_flag_rank(eq, wsum, &eq_tot);
+    const bool keep = prot || gt || (eq && eq_rank < need);
+    uint32_t keep_tot;
+    const uint32_t slot = written + block_flag_rank(keep, wsum, &keep_tot);
+    if (keep && slot < (uint32_t)K) out[slot] = i;
+    eq_seen += eq_tot;
+    written += keep_tot;
+  }
+  if (tid == 0) {
+    const bool ok = written == (uint32_t)K;
+    a.n_keep[b] = ok ? K : -1;
+    a.seq_status[b] = ok ? EPIKV_SEQ_OK : EPIKV_SEQ_RANGE;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_select, dim3(a.B), dim3(kSelectThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace epikv

@@ -1,0 +1,93 @@
+"""Shared helpers of the GPU parity tests: device transfers, paged-pool
+bookkeeping on the host, and configuration from a synthetic workload.
+
+Test infrastructure: it may use both the oracle and the HIP binding; the
+paging helpers here only move bytes around (the oracle sees logical rows).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import synth
+
+DEV = "cuda"
+
+
+def torch():
+    import torch as t
+    return t
+
+
+def dev(x: np.ndarray):
+    """Upload a numpy array (uint16 arrays travel as int16)."""
+    T = torch()
+    x = np.ascontiguousarray(x)
+    if x.dtype == np.uint16:
+        x = x.view(np.int16)
+    return T.from_numpy(x).to(DEV)
+
+
+def host(t) -> np.ndarray:
+    a = t.detach().cpu().numpy()
+    if a.dtype == np.int16:
+        a = a.view(np.uint16)
+    return a
+
+
+def cfg_for(E, w: synth.Workload, **kw):
+    """epikv_cfg for a workload (keyword overrides win)."""
+    c = E.default_cfg(
+        batch=w.B, hidden=w.hidden, n_layers=w.n_layers,
+        n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, page_size=w.page_size,
+        n_band_a=len(w.band_a), n_band_b=len(w.band_b), window=w.window,
+        budget=w.budget,
+        signal=E.SIGNAL_LAGKV if w.signal == "lagkv" else E.SIGNAL_HS,
+        smoothing=E.SMOOTH_MEAN if w.signal == "lagkv" else E.SMOOTH_Z)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def pool_shape(L, n_pages, page, H, d):
+    return (L, 2, n_pages, page, H * d)
+
+
+def gather_logical(pool_np: np.ndarray, pt_row: np.ndarray, n: int):
+    """Rows of positions 0..n-1 of one sequence: [L][2][n][H*d] (host)."""
+    page = pool_np.shape[3]
+    pos = np.arange(n)
+    pages = pt_row[pos // page]
+    slots = pos % page
+    return pool_np[:, :, pages, slots, :]
+
+
+def scatter_logical(pool_np: np.ndarray, pt_row: np.ndarray, first: int,
+                    rows: np.ndarray):
+    """Write rows [L][2][n][H*d] into positions first.. of one sequence."""
+    page = pool_np.shape[3]
+    pos = first + np.arange(rows.shape[2])
+    pool_np[:, :, pt_row[pos // page], pos % page, :] = rows
+
+
+def tie_exempt_compare(keep_gpu, keep_ref, scores_ref, n_prefix, N, K, R,
+                       tol=1e-3):
+    """Compare retained sets; positions that differ must sit within `tol`
+    of the oracle's cut score (the M-th best eligible score).  Returns the
+    number of exempted swaps."""
+    keep_gpu = np.asarray(keep_gpu)
+    keep_ref = np.asarray(keep_ref)
+    assert keep_gpu.size == keep_ref.size
+    assert np.all(np.diff(keep_gpu) > 0)
+    if np.array_equal(keep_gpu, keep_ref):
+        return 0
+    elig = np.arange(n_prefix, N - R)
+    kept_e = np.intersect1d(keep_ref, elig)
+    s = np.asarray(scores_ref, dtype=np.float64)
+    cut = np.min(s[kept_e])
+    diff = np.setxor1d(keep_gpu, keep_ref)
+    bound = tol * max(1.0, abs(cut))
+    for i in diff:
+        assert n_prefix <= i < N - R, f"protected position {i} differs"
+        assert abs(s[i] - cut) <= bound, \
+            f"position {i}: score {s[i]} vs cut {cut} (not a near tie)"
+    return diff.size // 2
