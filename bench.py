@@ -1,0 +1,387 @@
+"""Benchmark of the EpiKV eviction step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload ragged_batch32] [--no-cpu-baseline]
+
+One step = epikv_evict_step over one batch: score the new chunk of every
+sequence from its band-layer hidden states, z-score it, select the survivors
+and compact the paged KV cache (all 32 layers, K and V, 8 KV heads x 128).
+Inputs are seeded synthetic data resident in HBM before the timed region.
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = ("eviction steps/sec + achieved HBM GB/s (score+select+compact), "
+          "B=32, K=4096")
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Workload setup (device-resident)
+# ---------------------------------------------------------------------------
+class Setup:
+    pass
+
+
+def algorithmic_bytes(w: synth.Workload, lengths, n_keep):
+    """Bytes the step must move at least once (reads + writes), per stage.
+
+    score   : the chunk's band-layer rows, h_prev read + write, signal write
+    zscore  : signal read, carried ring read + write, scores write
+    select  : every cached score read once, keep_idx written
+    compact : per kept token, its K and V rows at every layer read and
+              written (2 * L * H * d * 2 bytes each way), plus its score and
+              position read and written
+    """
+    B, C, nb, D = w.B, w.chunk, w.n_band, w.hidden
+    row = w.kv_bytes_per_token
+    out = {}
+    out["score"] = B * nb * (C * D * 2 + 2 * D * 2 + C * 4)
+    out["zscore"] = B * nb * (C * 4 + 2 * (w.window - 1) * 4) + B * C * 4
+    out["select"] = int(np.sum(lengths)) * 4 + int(np.sum(n_keep)) * 4
+    out["compact"] = int(np.sum(n_keep)) * (2 * row + 2 * 8)
+    out["step"] = sum(out.values())
+    return out
+
+
+def setup_hs(w: synth.Workload, E, log_every=True):
+    """Build the headline (hidden-state signal) workload on the GPU."""
+    import torch
+    S = Setup()
+    g = synth.rng(w.seed)
+    lengths = synth.ragged_lengths(w, g)
+    S.lengths = lengths
+    B, C, D, nb = w.B, w.chunk, w.hidden, w.n_band
+    L, H, d, page = w.n_layers, w.n_kv_heads, w.head_dim, w.page_size
+    K = w.budget
+    t0 = time.time()
+    hid, before, _ = synth.hidden_chunk(w, g, lengths - C, C)
+    ring = synth.prior_samples(w, g, w.window - 1)
+    log(f"[setup] hidden states drawn in {time.time() - t0:.1f}s")
+    S.hidden_host = hid
+    S.before_host = before
+    S.ring_host = ring
+    ld_s = int(lengths.max())
+    S.ld_s = ld_s
+    scores = np.zeros((B, ld_s), dtype=np.float32)
+    S.old_scores = []
+    for b in range(B):
+        s = synth.old_scores(g, int(lengths[b]) - C)
+        scores[b, :s.size] = s
+        S.old_scores.append(s)
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dpp = (K + page - 1) // page
+    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    S.src_pt_host, S.dst_pt_host = src_pt, dst_pt
+
+    cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_kv_heads=H,
+                        head_dim=d, page_size=page,
+                        n_band_a=len(w.band_a), n_band_b=len(w.band_b),
+                        window=w.window, budget=K)
+    S.cfg = cfg
+    dev = torch.device("cuda")
+    S.hidden = torch.from_numpy(hid.view(np.int16)).to(dev)   # [nb][B][C][D]
+    S.hidden_ptrs = [S.hidden[l] for l in range(nb)]
+    st = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8)
+    sec = E.state_sections(cfg, st)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32))
+    sec["ring"][:] = torch.from_numpy(ring)
+    sec["h_prev"][:] = torch.from_numpy(before.transpose(1, 0, 2).copy()
+                                        .view(np.int16))
+    S.state_in = st.to(dev)
+    S.state_out = torch.zeros_like(S.state_in)
+    S.scores = torch.from_numpy(scores).to(dev)
+    S.dst_scores = torch.zeros_like(S.scores)
+    pos = np.tile(np.arange(ld_s, dtype=np.int32), (B, 1))
+    S.src_pos = torch.from_numpy(pos).to(dev)
+    S.dst_pos = torch.zeros_like(S.src_pos)
+    S.n_cached = torch.from_numpy(lengths.astype(np.int32)).to(dev)
+    S.n_prefix = torch.zeros(B, dtype=torch.int32, device=dev)
+    S.src_pt = torch.from_numpy(src_pt).to(dev)
+    S.dst_pt = torch.from_numpy(dst_pt).to(dev)
+    S.keep_idx = torch.zeros((B, K), dtype=torch.int32, device=dev)
+    S.n_keep = torch.zeros(B, dtype=torch.int32, device=dev)
+    S.status = torch.zeros(B, dtype=torch.int32, device=dev)
+    S.ws_bytes = E.workspace_bytes(cfg, C)
+    S.ws = torch.zeros(S.ws_bytes, dtype=torch.uint8, device=dev)
+
+    t0 = time.time()
+    row = H * d
+    S.src_pool = torch.empty((L, 2, n_src, page, row), dtype=torch.int16,
+                             device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed)
+    flat = S.src_pool.view(-1)
+    step = 1 << 30
+    for o in range(0, flat.numel(), step):
+        n = min(step, flat.numel() - o)
+        flat[o:o + n].random_(-32768, 32768, generator=gen)
+    S.dst_pool = torch.zeros((L, 2, n_dst, page, row), dtype=torch.int16,
+                             device=dev)
+    torch.cuda.synchronize()
+    log(f"[setup] pools: src {S.src_pool.numel() * 2 / 1e9:.1f} GB, "
+        f"dst {S.dst_pool.numel() * 2 / 1e9:.1f} GB filled in "
+        f"{time.time() - t0:.1f}s")
+    S.src = E.pool_of(S.src_pool.view(L, 2, n_src, page, H, d))
+    S.dst = E.pool_of(S.dst_pool.view(L, 2, n_dst, page, H, d))
+    S.io = E.make_step_io(
+        C, S.hidden_ptrs, D, C * D, S.n_cached, S.n_prefix, S.src, S.src_pt,
+        src_pt.shape[1], S.dst, S.dst_pt, dst_pt.shape[1], S.scores, ld_s,
+        S.state_in, S.state_out, S.keep_idx, S.n_keep, S.status, S.ws,
+        S.ws_bytes, dst_scores=S.dst_scores, src_pos=S.src_pos,
+        dst_pos=S.dst_pos)
+    S.sig = S.ws[:E.n_sig(cfg) * B * C * 4].view(torch.float32).view(
+        E.n_sig(cfg), B, C)
+    return S
+
+
+def run_stages(E, S, w, events=None):
+    """The four stages as separate C-ABI calls, events between them."""
+    C = w.chunk
+    if events:
+        events[0].record()
+    E.epikv_score(S.cfg, C, S.hidden_ptrs, w.hidden, C * w.hidden,
+                  state_in=S.state_in, state_out=S.state_out, sig=S.sig)
+    if events:
+        events[1].record()
+    E.epikv_zscore(S.cfg, C, S.sig, S.n_cached, S.state_in, S.state_out,
+                   S.scores, S.ld_s)
+    if events:
+        events[2].record()
+    E.epikv_select(S.cfg, S.scores, S.ld_s, S.n_cached, S.n_prefix,
+                   S.keep_idx, S.n_keep, S.status)
+    if events:
+        events[3].record()
+    E.epikv_compact(S.cfg, S.src, S.src_pt, S.src_pt.shape[1], S.dst,
+                    S.dst_pt, S.dst_pt.shape[1], S.keep_idx, S.n_keep,
+                    S.scores, S.dst_scores, S.src_pos, S.dst_pos, S.ld_s,
+                    S.status)
+    if events:
+        events[4].record()
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the same workload
+# ---------------------------------------------------------------------------
+def cpu_baseline(w: synth.Workload, S, budget_s: float = 12.0):
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(1)
+    except Exception:
+        limiter = None
+    g = synth.rng(w.seed + 1000)
+    C, nb = w.chunk, w.n_band
+    na = len(w.band_a)
+    spent = 0.0
+    done = 0
+    row_elems = w.n_kv_heads * w.head_dim
+    # source rows: random bits as on the GPU, a 2048-token block tiled to the
+    # longest sampled length (the oracle's work does not depend on content)
+    block = synth.random_bits16(g, (2048, w.n_layers, 2, row_elems))
+    n_max = int(S.lengths.max())
+    all_rows = np.concatenate([block] * ((n_max + 2047) // 2048))[:n_max]
+    del block
+    while done < w.B and spent < budget_s:
+        b = done
+        N = int(S.lengths[b])
+        rows = all_rows[:N]
+        hid = O.bf16_to_float64(S.hidden_host[:, b])        # [nb][C][D]
+        before = O.bf16_to_float64(S.before_host[:, b])     # [nb][D]
+        prior = [S.ring_host[b, l].astype(np.float64) for l in range(nb)]
+        scores = np.concatenate([S.old_scores[b].astype(np.float64),
+                                 np.zeros(C)])
+        t0 = time.perf_counter()
+        s_new, *_ = O.hs_chunk_scores(hid, before, prior, na, nb - na,
+                                      O.SMOOTH_Z, w.window, 1e-6)
+        scores[N - C:] = s_new
+        keep = O.select_keep(scores, 0, w.budget)
+        kept = O.compact_rows(rows, keep)
+        spent += time.perf_counter() - t0
+        done += 1
+        del kept
+    if limiter is not None:
+        limiter.unregister()
+    per_step = spent / done * w.B
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{done} of {w.B} sequences of the same step (score, "
+                      f"select, compact of all 32 layers) timed on one core; "
+                      f"scaled to the full batch ({spent:.1f}s measured)"}
+
+
+def copy_ceiling(n_bytes: int = 4 << 30, reps: int = 5):
+    """Device-to-device copy bandwidth (read + write bytes / time) of a plain
+    torch copy of n_bytes: the practical streaming ceiling on this GPU."""
+    import torch
+    a = torch.empty(n_bytes // 2, dtype=torch.int16, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        b.copy_(a)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms = np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])
+    del a, b
+    return 2 * n_bytes / (ms * 1e-3) / 1e9, float(ms)
+
+
+def traffic_from_profiles(kernel_src: str):
+    """HBM bytes per compact launch from the committed PMC summary, if it was
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "compact_ragged_batch32_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        digest = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+        if rec.get("kernel_sha256") != digest:
+            return None
+        return rec.get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="ragged_batch32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stages-only", action="store_true",
+                    help="only the per-stage loop (for profiling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not "
+              "supported (the eviction step is per-sequence and shards over "
+              "sequences without communication)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_26472_amd import epikv as E
+    E.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = synth.workload(args.workload)
+    if w.signal != "hs":
+        print("only hidden-state workloads are benchmarked", file=sys.stderr)
+        sys.exit(2)
+    log(f"[bench] workload {w.name}: B={w.B} K={w.budget} C={w.chunk}")
+    S = setup_hs(w, E)
+
+    # correctness guard: one step, every sequence must be OK with K kept
+    E.epikv_evict_step(S.cfg, S.io)
+    torch.cuda.synchronize()
+    st = S.status.cpu().numpy()
+    nk = S.n_keep.cpu().numpy()
+    assert np.all(st == 0) and np.all(nk == np.minimum(S.lengths, w.budget)), \
+        (st, nk)
+    ab = algorithmic_bytes(w, S.lengths, nk)
+
+    stream = torch.cuda.current_stream()
+    if not args.stages_only:
+        for _ in range(args.warmup):
+            E.epikv_evict_step(S.cfg, S.io)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            E.epikv_evict_step(S.cfg, S.io)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms_step = wall / args.steps * 1e3
+        log(f"[bench] evict_step: {ms_step:.3f} ms/step")
+    # per-stage durations with events on the launch stream
+    n_ev = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)]
+           for _ in range(n_ev)]
+    for _ in range(args.warmup):
+        run_stages(E, S, w)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(n_ev):
+        run_stages(E, S, w, evs[i])
+    torch.cuda.synchronize()
+    stage_wall = (time.perf_counter() - t0) / n_ev * 1e3
+    names = ["score", "zscore", "select", "compact"]
+    stage_ms = {n: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs]))
+                for k, n in enumerate(names)}
+    log("[bench] stages (ms): " + ", ".join(f"{k}={v:.4f}"
+                                          for k, v in stage_ms.items()))
+    if args.stages_only:
+        ms_step = stage_wall
+    copy_gbps, copy_ms = copy_ceiling()
+    log(f"[bench] device copy of 4 GiB: {copy_ms:.3f} ms = {copy_gbps:.0f} GB/s")
+    compact_gbps = ab["compact"] / (stage_ms["compact"] * 1e-3) / 1e9
+    step_gbps = ab["step"] / (ms_step * 1e-3) / 1e9
+    traffic = traffic_from_profiles(
+        os.path.join(ROOT, "paper_2606_26472_amd", "csrc", "compact.hip"))
+
+    result = {
+        "metric": METRIC,
+        "value": round(1e3 / ms_step, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "achieved_hbm_gbps": round(step_gbps, 1),
+        "config": {
+            "workload": f"{w.name}: batched eviction step, B={w.B} ragged "
+                        f"N in [{w.n_min},{w.n_max}], K={w.budget}, "
+                        f"C={w.chunk} new tokens, {w.n_layers} layers x "
+                        f"{w.n_kv_heads} KV heads x {w.head_dim} bf16 paged "
+                        f"({w.page_size}-token pages), HS bands 7-13/18-25, "
+                        f"z-score w={w.window}",
+            "B": w.B, "K": w.budget, "chunk": w.chunk,
+            "n_cached": [int(x) for x in S.lengths],
+            "algorithmic_bytes": ab,
+            "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        },
+        "roofline": {
+            "kernel": "k_compact",
+            "bound": "hbm",
+            "achieved": round(compact_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(compact_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "device_copy_gbps": round(copy_gbps, 1),
+            "frac_of_device_copy": round(compact_gbps / copy_gbps, 4),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample ...")
+        result["cpu_baseline"] = cpu_baseline(w, S)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

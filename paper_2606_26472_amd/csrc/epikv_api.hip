@@ -81,9 +81,9 @@ int check_cfg(const epikv_cfg* c) {
   const int hd = c->n_kv_heads * c->head_dim;
   if (hd > 2048) return EPIKV_EINVAL_SHAPE;
   const int row_vec = hd / 8;
-  // The compaction tile (one page of one plane) must fit the per-thread
-  // column budget of one workgroup.
-  if ((int64_t)c->page_size * row_vec > (int64_t)kCompactThreads * kCompactMaxVec) return EPIKV_EINVAL_SHAPE;
+  // One row of one plane must fit the per-thread column budget of a
+  // compaction workgroup.
+  if (row_vec > kCompactThreads * kCompactMaxVec) return EPIKV_EINVAL_SHAPE;
   if (c->signal == EPIKV_SIGNAL_LAGKV && (kScoreThreads % row_vec) != 0) return EPIKV_EINVAL_SHAPE;
   if (c->signal == EPIKV_SIGNAL_HS) {
     if (c->n_band_a < 1 || c->n_band_b < 0 || n_band(c) > EPIKV_MAX_BAND) return EPIKV_EINVAL_SHAPE;
@@ -328,8 +328,18 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.page_size = c->page_size;
   a.row_bytes = row_bytes(c);
   a.n_lk = 2 * c->n_layers;
-  a.lk_per_block = 8;
-  a.pages_per_seq = pages_for(c->budget, c->page_size);
+  // Tile: about 8 KiB of row data per plane (two 16-byte vectors per
+  // thread), at least one row, one plane per workgroup; measured best among
+  // 2..16 rows x 1..64 planes for 32 sequences
+  // keeping 4096 of 8k..32k tokens.
+  const int row_vec = row_bytes(c) / 16;
+  int rows = 2 * kCompactThreads / row_vec;
+  if (rows < 1) rows = 1;
+  if (rows > kCompactMaxRows) rows = kCompactMaxRows;
+  a.rows_per_block = rows;
+  a.lk_per_block = 1;
+  a.planes_together = 1;
+  a.blocks_per_seq = (c->budget + rows - 1) / rows;
   return a;
 }
 

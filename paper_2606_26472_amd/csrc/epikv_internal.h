@@ -106,7 +106,11 @@ struct CompactArgs {
   int32_t* dst_pos;
   int64_t ld_s;
   int32_t* seq_status;                     // optional
-  int32_t B, K, page_size, row_bytes, n_lk, lk_per_block, pages_per_seq;
+  int32_t B, K, page_size, row_bytes, n_lk;
+  int32_t rows_per_block;                  // destination slots per workgroup
+  int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
+  int32_t planes_together;                 // planes loaded before storing (1,2,4,8)
+  int32_t blocks_per_seq;                  // ceil(K / rows_per_block)
 };
 
 struct FillArgs {
@@ -133,6 +137,7 @@ constexpr int kZscoreTile = 256;         // tokens per zscore workgroup
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
 constexpr int kCompactMaxVec = 16;       // 16-byte vectors per thread per (layer, K|V)
+constexpr int kCompactMaxRows = 256;     // destination slots per compact workgroup
 constexpr int kLagMaxLds = 48 * 1024;
 
 }  // namespace epikv

@@ -97,20 +97,20 @@ class Workload:
 
 WORKLOADS = {
     # small replay: one sequence, 1024 tokens, evict every 64 to K=256
-    "c1": Workload("c1", 1, B=1, chunk=64, budget=256, n_min=320, n_max=320,
+    "drift_replay": Workload("drift_replay", 1, B=1, chunk=64, budget=256, n_min=320, n_max=320,
                    amplitude="drift", drift=0.001, trace_len=1024,
                    notes="drift replay"),
     # one 16k trace, lognormal deltas + 1% 8x spikes, evict every 128 to 4096
-    "c2": Workload("c2", 2, B=1, chunk=128, budget=4096, n_min=4224,
+    "spike_replay": Workload("spike_replay", 2, B=1, chunk=128, budget=4096, n_min=4224,
                    n_max=4224, trace_len=16384, notes="spike replay"),
     # headline: 32 ragged sequences 8k..32k, one batched step, K=4096
-    "c3": Workload("c3", 3, B=32, chunk=128, budget=4096, n_min=8192,
+    "ragged_batch32": Workload("ragged_batch32", 3, B=32, chunk=128, budget=4096, n_min=8192,
                    n_max=32768, notes="batched ragged step"),
     # Lag-KV: 8 sequences of 32k, chunk 256, K=8192
-    "c4": Workload("c4", 4, B=8, chunk=256, budget=8192, n_min=32768,
+    "lagkv_batch8": Workload("lagkv_batch8", 4, B=8, chunk=256, budget=8192, n_min=32768,
                    n_max=32768, signal="lagkv", notes="lag-kv step"),
     # one-shot scoring of a 65,536-token prefill, K=8192
-    "c5": Workload("c5", 5, B=1, chunk=65536, budget=8192, n_min=65536,
+    "prefill_64k": Workload("prefill_64k", 5, B=1, chunk=65536, budget=8192, n_min=65536,
                    n_max=65536, amplitude="drift_spikes", drift=0.0005,
                    notes="one-shot prefill"),
 }
@@ -275,5 +275,9 @@ def lagkv_channel_scale(w: Workload, g: np.random.Generator, chunk_idx: int):
 
 
 def random_bits16(g: np.random.Generator, shape) -> np.ndarray:
-    """Uniform 16-bit patterns (every bf16 value, NaNs included)."""
-    return g.integers(0, 1 << 16, size=shape, dtype=np.uint16)
+    """Uniform 16-bit patterns (every bf16 value, NaNs included): uniform
+    64-bit integers cut into four 16-bit words."""
+    n = int(np.prod(shape))
+    raw = g.integers(0, np.iinfo(np.uint64).max, size=(n + 3) // 4,
+                     dtype=np.uint64, endpoint=True)
+    return raw.view(np.uint16)[:n].reshape(shape)

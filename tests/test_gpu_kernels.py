@@ -300,7 +300,7 @@ def test_lagkv_matches_oracle(E):
     pt, n_pages = synth.page_tables(Ns, page, g)
     pool = np.zeros((L, 2, n_pages, page, H * d), dtype=np.uint16)
     tok = []   # logical rows per sequence [N][L][2][H*d]
-    wl = synth.workload("c4", B=B, n_layers=L)
+    wl = synth.workload("lagkv_batch8", B=B, n_layers=L)
     for b in range(B):
         chunks = [synth.kv_rows(g, (C, L, 2, H, d),
                                 synth.lagkv_channel_scale(wl, g, j))
