@@ -86,9 +86,11 @@ def setup_hs(w: synth.Workload, E, log_every=True):
         s = synth.old_scores(g, int(lengths[b]) - C)
         scores[b, :s.size] = s
         S.old_scores.append(s)
+    # The cache being evicted has its pages scattered over the pool (a random
+    # permutation: the fragmented state of a long-running allocator); the
+    # rebuilt cache gets one contiguous run of ceil(K/16) pages per sequence.
     src_pt, n_src = synth.page_tables(lengths, page, g)
-    dpp = (K + page - 1) // page
-    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    dst_pt, n_dst = synth.contiguous_page_tables(np.full(B, K), page)
     S.src_pt_host, S.dst_pt_host = src_pt, dst_pt
 
     cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_kv_heads=H,
@@ -121,6 +123,8 @@ def setup_hs(w: synth.Workload, E, log_every=True):
     S.status = torch.zeros(B, dtype=torch.int32, device=dev)
     S.ws_bytes = E.workspace_bytes(cfg, C)
     S.ws = torch.zeros(S.ws_bytes, dtype=torch.uint8, device=dev)
+    S.cws_bytes = E.compact_workspace_bytes(cfg)
+    S.cws = torch.zeros(S.cws_bytes, dtype=torch.uint8, device=dev)
 
     t0 = time.time()
     row = H * d
@@ -172,7 +176,7 @@ def run_stages(E, S, w, events=None):
     E.epikv_compact(S.cfg, S.src, S.src_pt, S.src_pt.shape[1], S.dst,
                     S.dst_pt, S.dst_pt.shape[1], S.keep_idx, S.n_keep,
                     S.scores, S.dst_scores, S.src_pos, S.dst_pos, S.ld_s,
-                    S.status)
+                    S.status, S.cws, S.cws_bytes)
     if events:
         events[4].record()
 

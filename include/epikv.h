@@ -155,9 +155,13 @@ size_t epikv_state_bytes(const epikv_cfg* cfg);
  * Returns EPIKV_OK or a host error code. */
 int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]);
 
-/* Device scratch that epikv_score and epikv_evict_step need for a chunk of
- * `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
+/* Device scratch that epikv_evict_step (and epikv_score) needs for a chunk
+ * of `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
+
+/* Device scratch of epikv_compact: 16 bytes per (sequence, kept slot),
+ * B*K*16 rounded up to 256.  0 for an invalid cfg. */
+size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg);
 
 /* Reset a state buffer of epikv_state_bytes(cfg) bytes to the start of a
  * stream (every section zero).  Uses a fill kernel, so it may be captured
@@ -252,6 +256,9 @@ int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
  * (not checked), and dst_scores/dst_pos must not overlap their sources.
  * Rows whose index or page id is out of range are skipped and set
  * seq_status[b] = RANGE when seq_status is given.
+ * workspace: 16-byte aligned device scratch of at least
+ * epikv_compact_workspace_bytes(cfg) bytes (the resolved row offsets); it
+ * must not overlap any other argument.
  */
 int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src,
                   const int32_t* src_pt, int64_t ld_src_pt,
@@ -259,7 +266,8 @@ int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src,
                   int64_t ld_dst_pt, const int32_t* keep_idx,
                   const int32_t* n_keep, const float* src_scores,
                   float* dst_scores, const int32_t* src_pos, int32_t* dst_pos,
-                  int64_t ld_s, int32_t* seq_status, hipStream_t stream);
+                  int64_t ld_s, int32_t* seq_status, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream);
 
 /* Arguments of one eviction step (host struct; pointers as above). */
 typedef struct epikv_step_io {

@@ -4,96 +4,97 @@
 // (layer, K|V) holds all KV heads (n_kv_heads * head_dim bf16, 2 KiB for
 // 8 x 128), so the copy is a gather of 2 KiB rows: pure HBM streaming.
 //
-// One 256-thread workgroup owns rows_per_block consecutive destination
-// slots of one sequence for lk_per_block (layer, K|V) planes.  The slots'
-// source and destination row offsets are resolved once (keep_idx -> page
-// tables) into LDS; each thread then holds NV 16-byte columns of the
-// rows x row_bytes tile and reuses their offsets for every plane.  Small
-// tiles (one or two 16-byte vectors per thread) keep many workgroups in
-// flight on every CU, which is what lets a streaming copy approach the HBM
-// rate on gfx950.  Loads and stores are non-temporal: each byte is touched
-// once.
+// Two kernels:
+//   resolve  one thread per kept slot turns keep_idx and the two page tables
+//            into the byte offsets of the source and destination rows inside
+//            a plane (one 16-byte record per slot, in the workspace), and
+//            copies the slot's score and position;
+//   gather   a 256-thread workgroup owns rows_per_block consecutive slots of
+//            one sequence for lk_per_block planes.  Each thread loads the
+//            offset record of its row and then streams its NV 16-byte
+//            columns of every plane: one dependent load before the data,
+//            so short-lived workgroups keep HBM busy.  Loads and stores are
+//            non-temporal: each byte is touched once.
 #include "epikv_internal.h"
 
 namespace epikv {
 namespace {
 
-template <int NV, int PL>
-__global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
-  __shared__ int64_t soff[kCompactMaxRows];
-  __shared__ int64_t doff[kCompactMaxRows];
-  __shared__ int bad;
-  const int tid = threadIdx.x;
-  const int b = blockIdx.x / a.blocks_per_seq;
-  const int cb = blockIdx.x - b * a.blocks_per_seq;
+__global__ __launch_bounds__(kCompactThreads) void k_compact_resolve(CompactArgs a) {
+  const int j = blockIdx.x * kCompactThreads + threadIdx.x;
+  const int b = blockIdx.y;
   // A caller's n_keep above K is clamped so keep_idx is never read past the
   // sequence's row.
   const int nk = min(a.n_keep[b], a.K);
-  const int j0 = cb * a.rows_per_block;
-  if (nk <= j0) return;  // also n_keep < 0: sequence untouched
-  const int rows = min(a.rows_per_block, nk - j0);
-
-  if (tid == 0) bad = 0;
-  __syncthreads();
-  for (int r = tid; r < rows; r += kCompactThreads) {
-    const int j = j0 + r;
-    const int idx = a.keep_idx[(int64_t)b * a.K + j];
-    int64_t so = -1, dso = -1;
-    if (idx >= 0) {
-      const int sp = idx / a.page_size;
-      const int slot = idx - sp * a.page_size;
-      if ((int64_t)sp < a.ld_src_pt) {
-        const int pg = a.src_pt[(int64_t)b * a.ld_src_pt + sp];
-        if (pg >= 0 && pg < a.s_npages)
-          so = (int64_t)pg * a.s_page + (int64_t)slot * a.row_bytes;
-      }
-    }
-    {
-      const int dp = j / a.page_size;
-      const int dslot = j - dp * a.page_size;
-      if ((int64_t)dp < a.ld_dst_pt) {
-        const int pg = a.dst_pt[(int64_t)b * a.ld_dst_pt + dp];
-        if (pg >= 0 && pg < a.d_npages)
-          dso = (int64_t)pg * a.d_page + (int64_t)dslot * a.row_bytes;
-      }
-    }
-    const bool ok = so >= 0 && dso >= 0;
-    soff[r] = ok ? so : -1;
-    doff[r] = dso;
-    if (!ok) bad = 1;
-    if (blockIdx.y == 0 && ok && (int64_t)idx < a.ld_s && (int64_t)j < a.ld_s) {
-      const int64_t si = (int64_t)b * a.ld_s + idx;
-      const int64_t di = (int64_t)b * a.ld_s + j;
-      if (a.dst_scores) a.dst_scores[di] = a.src_scores[si];
-      if (a.dst_pos) a.dst_pos[di] = a.src_pos[si];
+  if (j >= nk) return;  // also n_keep < 0: sequence untouched
+  const int idx = a.keep_idx[(int64_t)b * a.K + j];
+  int64_t so = -1, dso = -1;
+  if (idx >= 0) {
+    const int sp = idx / a.page_size;
+    const int slot = idx - sp * a.page_size;
+    if ((int64_t)sp < a.ld_src_pt) {
+      const int pg = a.src_pt[(int64_t)b * a.ld_src_pt + sp];
+      if (pg >= 0 && pg < a.s_npages) so = (int64_t)pg * a.s_page + (int64_t)slot * a.row_bytes;
     }
   }
-  __syncthreads();
-  if (bad && a.seq_status && tid == 0) a.seq_status[b] = EPIKV_SEQ_RANGE;
+  {
+    const int dp = j / a.page_size;
+    const int dslot = j - dp * a.page_size;
+    if ((int64_t)dp < a.ld_dst_pt) {
+      const int pg = a.dst_pt[(int64_t)b * a.ld_dst_pt + dp];
+      if (pg >= 0 && pg < a.d_npages) dso = (int64_t)pg * a.d_page + (int64_t)dslot * a.row_bytes;
+    }
+  }
+  const bool ok = so >= 0 && dso >= 0;
+  int64_t* rec = a.offsets + 2 * ((int64_t)b * a.K + j);
+  rec[0] = ok ? so : -1;
+  rec[1] = ok ? dso : -1;
+  if (!ok) {
+    if (a.seq_status) a.seq_status[b] = EPIKV_SEQ_RANGE;
+    return;
+  }
+  if ((int64_t)idx < a.ld_s && (int64_t)j < a.ld_s) {
+    const int64_t si = (int64_t)b * a.ld_s + idx;
+    const int64_t di = (int64_t)b * a.ld_s + j;
+    if (a.dst_scores) a.dst_scores[di] = a.src_scores[si];
+    if (a.dst_pos) a.dst_pos[di] = a.src_pos[si];
+  }
+}
 
-  // This thread's NV columns of the rows x row_vec tile; the offsets are the
-  // same for every plane.
+template <int NV, int PL>
+__global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x / a.blocks_per_seq;
+  const int cb = blockIdx.x - b * a.blocks_per_seq;
+  const int j0 = cb * a.rows_per_block;
   const int row_vec = a.row_bytes >> 4;
-  const int nvec = rows * row_vec;
+  // The offset records of slots < K are always readable, so they are loaded
+  // alongside n_keep rather than after it.
   int64_t so[NV];
   int64_t dof[NV];
+  int jr[NV];
 #pragma unroll
   for (int q = 0; q < NV; ++q) {
     const int v = tid + q * kCompactThreads;
+    const int r = v / row_vec;
+    const int j = j0 + r;
+    jr[q] = (r < a.rows_per_block && j < a.K) ? j : -1;
     so[q] = -1;
     dof[q] = 0;
-    if (v < nvec) {
-      const int r = v / row_vec;
+    if (jr[q] >= 0) {
       const int64_t col = (int64_t)(v - r * row_vec) * 16;
-      if (soff[r] >= 0) {
-        so[q] = soff[r] + col;
-        dof[q] = doff[r] + col;
-      }
+      const u32x4 rec = *reinterpret_cast<const u32x4*>(a.offsets + 2 * ((int64_t)b * a.K + j));
+      const int64_t s0 = (int64_t)(((uint64_t)rec[1] << 32) | rec[0]);
+      const int64_t d0 = (int64_t)(((uint64_t)rec[3] << 32) | rec[2]);
+      so[q] = s0 >= 0 ? s0 + col : -1;
+      dof[q] = d0 + col;
     }
   }
+  const int nk = min(a.n_keep[b], a.K);
+#pragma unroll
+  for (int q = 0; q < NV; ++q)
+    if (jr[q] >= nk) so[q] = -1;
 
-  // PL planes are loaded together before any of them is stored, so each
-  // thread keeps PL * NV independent 16-byte loads in flight.
   const int lk0 = blockIdx.y * a.lk_per_block;
   const int lk1 = min(a.n_lk, lk0 + a.lk_per_block);
   for (int lk = lk0; lk < lk1; lk += PL) {
@@ -143,6 +144,10 @@ hipError_t launch_nv(const CompactArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_compact_resolve, dim3((a.K + kCompactThreads - 1) / kCompactThreads, a.B),
+                     dim3(kCompactThreads), 0, s, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   switch (a.planes_together) {
     case 1: return launch_nv<1>(a, s);
     case 2: return launch_nv<2>(a, s);

@@ -60,6 +60,10 @@ size_t sig_bytes(const epikv_cfg* c, int chunk) {
   return align_up(4 * (size_t)n_sig(c) * (size_t)c->batch * (size_t)chunk);
 }
 
+size_t compact_ws_bytes(const epikv_cfg* c) {
+  return align_up(16 * (size_t)c->batch * (size_t)c->budget);
+}
+
 size_t partial_bytes(const epikv_cfg* c, int chunk) {
   if (c->signal != EPIKV_SIGNAL_LAGKV) return 0;
   return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk);
@@ -277,9 +281,12 @@ SelectArgs select_args(const epikv_cfg* c, const float* scores, int64_t ld_s, co
 int check_compact(const epikv_cfg* c, const epikv_pool* src, const int32_t* src_pt, int64_t ld_src_pt,
                   const epikv_pool* dst, const int32_t* dst_pt, int64_t ld_dst_pt,
                   const int32_t* keep_idx, const int32_t* n_keep, const float* src_scores,
-                  float* dst_scores, const int32_t* src_pos, int32_t* dst_pos, int64_t ld_s) {
+                  float* dst_scores, const int32_t* src_pos, int32_t* dst_pos, int64_t ld_s,
+                  const void* ws, size_t ws_bytes) {
   int st = check_cfg(c);
   if (st) return st;
+  if (!ws || ws_bytes < compact_ws_bytes(c)) return EPIKV_EWORKSPACE;
+  if (!aligned16(ws)) return EPIKV_EALIGN;
   st = check_pool(src);
   if (st) return st;
   st = check_pool(dst);
@@ -299,7 +306,7 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
                          int64_t ld_src_pt, const epikv_pool* dst, const int32_t* dst_pt,
                          int64_t ld_dst_pt, const int32_t* keep_idx, const int32_t* n_keep,
                          const float* src_scores, float* dst_scores, const int32_t* src_pos,
-                         int32_t* dst_pos, int64_t ld_s, int32_t* seq_status) {
+                         int32_t* dst_pos, int64_t ld_s, int32_t* seq_status, void* ws) {
   CompactArgs a;
   a.src = (const char*)src->base;
   a.s_layer = src->stride_layer;
@@ -323,6 +330,7 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.dst_pos = dst_pos;
   a.ld_s = ld_s;
   a.seq_status = seq_status;
+  a.offsets = (int64_t*)ws;
   a.B = c->batch;
   a.K = c->budget;
   a.page_size = c->page_size;
@@ -417,7 +425,12 @@ EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]) {
 
 EPIKV_EXPORT size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk) {
   if (check_cfg(cfg) || chunk < 1) return 0;
-  return sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk);
+  return sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk) + compact_ws_bytes(cfg);
+}
+
+EPIKV_EXPORT size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg) {
+  if (check_cfg(cfg)) return 0;
+  return compact_ws_bytes(cfg);
 }
 
 EPIKV_EXPORT int epikv_state_init(const epikv_cfg* cfg, void* state, hipStream_t stream) {
@@ -468,13 +481,14 @@ EPIKV_EXPORT int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src, cons
                                int64_t ld_dst_pt, const int32_t* keep_idx, const int32_t* n_keep,
                                const float* src_scores, float* dst_scores, const int32_t* src_pos,
                                int32_t* dst_pos, int64_t ld_s, int32_t* seq_status,
-                               hipStream_t stream) {
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
   const int st = check_compact(cfg, src, src_pt, ld_src_pt, dst, dst_pt, ld_dst_pt, keep_idx, n_keep,
-                               src_scores, dst_scores, src_pos, dst_pos, ld_s);
+                               src_scores, dst_scores, src_pos, dst_pos, ld_s, workspace,
+                               workspace_bytes);
   if (st) return st;
   return launched(launch_compact(compact_args(cfg, src, src_pt, ld_src_pt, dst, dst_pt, ld_dst_pt,
                                               keep_idx, n_keep, src_scores, dst_scores, src_pos,
-                                              dst_pos, ld_s, seq_status),
+                                              dst_pos, ld_s, seq_status, workspace),
                                  stream));
 }
 
@@ -496,17 +510,19 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   st = check_select(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix, io->keep_idx, io->n_keep,
                     io->seq_status);
   if (st) return st;
+  char* ws = (char*)io->workspace;
+  char* ws_offsets = ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk);
   st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
                      io->keep_idx, io->n_keep, io->scores, io->dst_scores, io->src_pos, io->dst_pos,
-                     io->ld_s);
+                     io->ld_s, ws_offsets, compact_ws_bytes(cfg));
   if (st) return st;
   const size_t ws_state = state_layout(cfg).total;
   if (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
       overlap(io->workspace, io->workspace_bytes, io->state_out, ws_state))
     return EPIKV_EALIAS;
 
-  float* sig = (float*)io->workspace;
-  float* partial = (float*)((char*)io->workspace + sig_bytes(cfg, io->chunk));
+  float* sig = (float*)ws;
+  float* partial = (float*)(ws + sig_bytes(cfg, io->chunk));
   st = run_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
                  io->ld_src_pt, io->n_cached, io->state_in, io->state_out, sig, partial, stream);
   if (st) return st;
@@ -522,6 +538,6 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   return launched(launch_compact(
       compact_args(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
                    io->keep_idx, io->n_keep, with_scores ? io->scores : nullptr, io->dst_scores,
-                   io->src_pos, io->dst_pos, io->ld_s, io->seq_status),
+                   io->src_pos, io->dst_pos, io->ld_s, io->seq_status, ws_offsets),
       stream));
 }

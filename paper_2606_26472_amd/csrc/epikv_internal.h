@@ -106,6 +106,7 @@ struct CompactArgs {
   int32_t* dst_pos;
   int64_t ld_s;
   int32_t* seq_status;                     // optional
+  int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
   int32_t B, K, page_size, row_bytes, n_lk;
   int32_t rows_per_block;                  // destination slots per workgroup
   int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
@@ -133,7 +134,8 @@ hipError_t launch_fill(const FillArgs& a, hipStream_t s);
 // Tunables the host layer validates against.
 constexpr int kScoreThreads = 256;
 constexpr int kScoreSeg = 32;            // tokens per score_hs workgroup
-constexpr int kZscoreTile = 256;         // tokens per zscore workgroup
+constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per lane)
+constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
 constexpr int kCompactMaxVec = 16;       // 16-byte vectors per thread per (layer, K|V)

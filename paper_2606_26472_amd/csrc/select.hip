@@ -16,8 +16,9 @@
 //      prefix count ranks the keys equal to T by position (the first `need`
 //      of them are kept) and a second one gives every kept position its
 //      output slot, so keep_idx comes out ascending without a sort.
-// Scores are re-read from global memory in each pass (they stay in L2),
-// so N is not limited by LDS.
+// For N up to 64 Ki positions every thread keeps the keys of its positions
+// (tid, tid+1024, ...) in registers for all four sweeps; longer sequences
+// re-read the scores from global memory (L2) in each sweep.
 #include "epikv_internal.h"
 
 namespace epikv {
@@ -70,6 +71,9 @@ __device__ __forceinline__ uint32_t block_flag_rank(bool flag, uint32_t* wsum, u
   return pre + below;
 }
 
+// KPT > 0: positions tid + k*1024 (k < KPT) have their keys in registers.
+// KPT == 0: keys are recomputed from global memory in every sweep.
+template <int KPT>
 __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
   __shared__ uint32_t hist[2048];
   __shared__ uint32_t wsum[kWaves];
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
   const int R = a.R;
   int32_t* out = a.keep_idx + (int64_t)b * K;
 
-  if (N < a.min_n || (int64_t)N > a.ld_s || P < 0) {
+  if (N < a.min_n || (int64_t)N > a.ld_s || P < 0 || (KPT > 0 && N > KPT * kSelectThreads)) {
     if (tid == 0) {
       a.n_keep[b] = -1;
       a.seq_status[b] = EPIKV_SEQ_RANGE;
@@ -107,8 +111,17 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
 
   const float* s = a.scores + (int64_t)b * a.ld_s;
   const int lo = P, hi = N - R;  // eligible positions [lo, hi)
+  constexpr int KR = KPT > 0 ? KPT : 1;
+  uint32_t keys[KR];
+  if (KPT > 0) {
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+      const int i = tid + k * kSelectThreads;
+      keys[k] = (i >= lo && i < hi) ? rank_key(s[i]) : 0u;
+    }
+  }
   uint32_t prefix = 0u, mask = 0u;
-  uint32_t k = (uint32_t)(K - P - R);  // rank (1-based) of the threshold key
+  uint32_t need = (uint32_t)(K - P - R);  // rank (1-based) of the threshold key
 
   const int shifts[3] = {21, 10, 0};
   const int nbits[3] = {11, 11, 10};
@@ -119,9 +132,18 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
     const uint32_t dmask = (uint32_t)nb - 1u;
     for (int i = tid; i < nb; i += kSelectThreads) hist[i] = 0u;
     __syncthreads();
-    for (int i = lo + tid; i < hi; i += kSelectThreads) {
-      const uint32_t key = rank_key(s[i]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
+    if (KPT > 0) {
+#pragma unroll
+      for (int k = 0; k < KR; ++k) {
+        const int i = tid + k * kSelectThreads;
+        if (i >= lo && i < hi && (keys[k] & mask) == prefix)
+          atomicAdd(&hist[(keys[k] >> shift) & dmask], 1u);
+      }
+    } else {
+      for (int i = lo + tid; i < hi; i += kSelectThreads) {
+        const uint32_t key = rank_key(s[i]);
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
+      }
     }
     __syncthreads();
     // Thread t owns the bpt bins just below nb - t*bpt (descending order),
@@ -132,12 +154,12 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
     for (int q = 0; q < bpt; ++q) local += hist[top - q];
     const uint32_t incl = block_inclusive_scan(local, wsum);
     const uint32_t excl = incl - local;
-    if (excl < k && k <= incl) {
+    if (excl < need && need <= incl) {
       uint32_t above = excl;
       int d = top - bpt + 1;
       for (int q = 0; q < bpt; ++q) {
         const uint32_t h = hist[top - q];
-        if (above + h >= k) {
+        if (above + h >= need) {
           d = top - q;
           break;
         }
@@ -149,19 +171,30 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
     __syncthreads();
     prefix |= sel_digit << shift;
     mask |= dmask << shift;
-    k -= sel_above;
+    need -= sel_above;
     __syncthreads();
   }
 
+  // need = keys equal to T that are kept, lowest positions first.
   const uint32_t T = prefix;
-  const uint32_t need = k;  // keys equal to T that are kept, lowest positions first
   uint32_t eq_seen = 0u, written = 0u;
-  for (int t0 = 0; t0 < N; t0 += kSelectThreads) {
-    const int i = t0 + tid;
+  const int tiles = (N + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+  for (int t = 0; t < tiles; ++t) {
+    const int i = t * kSelectThreads + tid;
     const bool valid = i < N;
     const bool prot = valid && (i < lo || i >= hi);
     const bool elig = valid && !prot;
-    const uint32_t key = elig ? rank_key(s[i]) : 0u;
+    uint32_t key = 0u;
+    if (elig) {
+      if (KPT > 0) {
+#pragma unroll
+        for (int k = 0; k < KR; ++k)
+          if (k == t) key = keys[k];
+      } else {
+        key = rank_key(s[i]);
+      }
+    }
     const bool gt = elig && key > T;
     const bool eq = elig && key == T;
     uint32_t eq_tot;
@@ -180,11 +213,26 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
   }
 }
 
+template <int KPT>
+hipError_t launch(const SelectArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((k_select<KPT>), dim3(a.B), dim3(kSelectThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_select, dim3(a.B), dim3(kSelectThreads), 0, s, a);
-  return hipGetLastError();
+  // Registers per thread for the keys: the smallest power of two covering
+  // ld_s positions (every N is at most ld_s).
+  const int64_t per = (a.ld_s + kSelectThreads - 1) / kSelectThreads;
+  if (per <= 1) return launch<1>(a, s);
+  if (per <= 2) return launch<2>(a, s);
+  if (per <= 4) return launch<4>(a, s);
+  if (per <= 8) return launch<8>(a, s);
+  if (per <= 16) return launch<16>(a, s);
+  if (per <= 32) return launch<32>(a, s);
+  if (per <= 64) return launch<64>(a, s);
+  return launch<0>(a, s);
 }
 
 }  // namespace epikv

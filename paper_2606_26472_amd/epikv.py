@@ -9,7 +9,6 @@ from __future__ import annotations
 
 import ctypes
 import os
-from dataclasses import dataclass
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libepikv.so")
@@ -37,7 +36,8 @@ MAX_BAND = 32
 
 EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_state_bytes", "epikv_state_layout",
-            "epikv_workspace_bytes", "epikv_state_init", "epikv_score",
+            "epikv_workspace_bytes", "epikv_compact_workspace_bytes",
+            "epikv_state_init", "epikv_score",
             "epikv_zscore", "epikv_select", "epikv_compact",
             "epikv_evict_step")
 
@@ -107,13 +107,14 @@ def lib() -> ctypes.CDLL:
         "epikv_state_bytes": (sz, [cfgp]),
         "epikv_state_layout": (ctypes.c_int, [cfgp, ctypes.POINTER(sz)]),
         "epikv_workspace_bytes": (sz, [cfgp, i32]),
+        "epikv_compact_workspace_bytes": (sz, [cfgp]),
         "epikv_state_init": (ctypes.c_int, [cfgp, P, P]),
         "epikv_score": (ctypes.c_int, [cfgp, i32, ctypes.POINTER(P), i64, i64,
                                        poolp, P, i64, P, P, P, P, P, sz, P]),
         "epikv_zscore": (ctypes.c_int, [cfgp, i32, P, P, P, P, P, i64, P, P]),
         "epikv_select": (ctypes.c_int, [cfgp, P, i64, P, P, P, P, P, P]),
         "epikv_compact": (ctypes.c_int, [cfgp, poolp, P, i64, poolp, P, i64,
-                                         P, P, P, P, P, P, i64, P, P]),
+                                         P, P, P, P, P, P, i64, P, P, sz, P]),
         "epikv_evict_step": (ctypes.c_int, [cfgp, ctypes.POINTER(StepIO), P]),
     }
     for name, (res, args) in sig.items():
@@ -181,12 +182,8 @@ def workspace_bytes(cfg: Cfg, chunk: int) -> int:
     return int(lib().epikv_workspace_bytes(ctypes.byref(cfg), int(chunk)))
 
 
-@dataclass
-class PoolView:
-    """A paged pool held in a tensor of shape [L][2][n_pages][page][H][d]
-    (bf16 or int16 storage); `pool` is the C descriptor."""
-    tensor: object
-    pool: Pool
+def compact_workspace_bytes(cfg: Cfg) -> int:
+    return int(lib().epikv_compact_workspace_bytes(ctypes.byref(cfg)))
 
 
 def pool_of(t) -> Pool:
@@ -245,12 +242,14 @@ def epikv_select(cfg: Cfg, scores, ld_s, n_cached, n_prefix, keep_idx,
 def epikv_compact(cfg: Cfg, src: Pool, src_pt, ld_src_pt, dst: Pool, dst_pt,
                   ld_dst_pt, keep_idx, n_keep, src_scores=None,
                   dst_scores=None, src_pos=None, dst_pos=None, ld_s=0,
-                  seq_status=None, stream=None):
+                  seq_status=None, workspace=None, workspace_bytes_=0,
+                  stream=None):
     _check(lib().epikv_compact(
         ctypes.byref(cfg), ctypes.byref(src), _ptr(src_pt), int(ld_src_pt),
         ctypes.byref(dst), _ptr(dst_pt), int(ld_dst_pt), _ptr(keep_idx),
         _ptr(n_keep), _ptr(src_scores), _ptr(dst_scores), _ptr(src_pos),
-        _ptr(dst_pos), int(ld_s), _ptr(seq_status), _stream(stream)),
+        _ptr(dst_pos), int(ld_s), _ptr(seq_status), _ptr(workspace),
+        int(workspace_bytes_), _stream(stream)),
         "epikv_compact")
 
 

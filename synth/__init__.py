@@ -255,6 +255,23 @@ def page_tables(lengths, page_size: int, g: np.random.Generator,
     return table, n_pages_total
 
 
+def contiguous_page_tables(lengths, page_size: int, first: int = 0,
+                           ld: int | None = None):
+    """Each sequence gets one contiguous run of pages, sequences one after
+    another (the allocation of a freshly rebuilt cache).  Returns
+    (table int32 [B][ld] padded with -1, n_pages_total)."""
+    lengths = np.asarray(lengths, dtype=np.int64)
+    need = (lengths + page_size - 1) // page_size
+    if ld is None:
+        ld = int(need.max()) if need.size else 1
+    table = np.full((lengths.size, ld), -1, dtype=np.int32)
+    o = first
+    for b, k in enumerate(need):
+        table[b, :k] = np.arange(o, o + k)
+        o += k
+    return table, int(o)
+
+
 def kv_rows(g: np.random.Generator, shape, scale=None) -> np.ndarray:
     """bf16 patterns of N(0,1) values (optionally times a broadcastable
     per-channel scale)."""

@@ -92,6 +92,9 @@ def test_state_layout_sizes(E):
     assert E.workspace_bytes(c, 128) >= 4 * 15 * 32 * 128
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
     assert E.workspace_bytes(c, 0) == 0
+    assert E.compact_workspace_bytes(c) == 16 * 32 * 4096
+    assert E.workspace_bytes(c, 128) >= E.compact_workspace_bytes(c) \
+        + 4 * 15 * 32 * 128
 
 
 def test_strerror_covers_every_code(E):
@@ -167,20 +170,31 @@ def test_zscore_select_compact_validation(E):
     src = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
     dst = E.Pool(2 * A, 1 << 30, 1 << 29, 32768, 100)
     bad = E.Pool(None, 0, 0, 0, 0)
+    W = 4 * A
     assert cp(ctypes.byref(c), ctypes.byref(bad), A, 4, ctypes.byref(dst), A,
-              16, A, A, None, None, None, None, 0, None,
+              16, A, A, None, None, None, None, 0, None, W, 1 << 20,
               None) == E.EPIKV_EINVAL_NULL
+    # workspace missing, too small, misaligned
+    assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
+              16, A, A, None, None, None, None, 0, None, None, 0,
+              None) == E.EPIKV_EWORKSPACE
+    assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
+              16, A, A, None, None, None, None, 0, None, W, 64,
+              None) == E.EPIKV_EWORKSPACE
+    assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
+              16, A, A, None, None, None, None, 0, None, W + 8, 1 << 20,
+              None) == E.EPIKV_EALIGN
     # destination page table narrower than ceil(K / page_size)
     assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
-              15, A, A, None, None, None, None, 0, None,
+              15, A, A, None, None, None, None, 0, None, W, 1 << 20,
               None) == E.EPIKV_EINVAL_SHAPE
     # scores given on one side only
     assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
-              16, A, A, A, None, None, None, 100, None,
+              16, A, A, A, None, None, None, 100, None, W, 1 << 20,
               None) == E.EPIKV_EINVAL_NULL
     # in-place score compaction
     assert cp(ctypes.byref(c), ctypes.byref(src), A, 4, ctypes.byref(dst), A,
-              16, A, A, A, A + 64, None, None, 100, None,
+              16, A, A, A, A + 64, None, None, 100, None, W, 1 << 20,
               None) == E.EPIKV_EALIAS
 
 

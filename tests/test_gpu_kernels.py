@@ -160,15 +160,18 @@ def test_zscore_matches_oracle(E, mode, C):
 # ---------------------------------------------------------------------------
 # select: Sec. 3.1, Sec. 3.3, App. D
 # ---------------------------------------------------------------------------
-def test_select_matches_oracle_bit_exact(E):
+@pytest.mark.parametrize("ld_s", [65536, 80000, 3000])
+def test_select_matches_oracle_bit_exact(E, ld_s):
     import torch
-    print("select", flush=True)
-    g = synth.rng(300)
+    print(f"select ld_s={ld_s}", flush=True)
+    g = synth.rng(300 + ld_s)
     K = 1024
-    Ns = [0, 37, 1024, 1025, 1500, 5000, 32768, 65536, 70000, 4000, 2048]
-    Ps = [0, 0, 3, 0, 17, 100, 0, 64, 0, 1000, 896]
+    # ld_s picks the kernel variant: keys in registers (<= 64 Ki positions)
+    # or re-read from memory in every sweep (longer rows)
+    Ns = [0, 37, 1024, 1025, 1500, 5000, 32768, 65536, 70000, 4000, 2048,
+          ld_s, ld_s + 1, 2049]
+    Ps = [0, 0, 3, 0, 17, 100, 0, 64, 0, 1000, 896, 5, 0, 0]
     B = len(Ns)
-    ld_s = 65536
     sc = np.zeros((B, ld_s), dtype=np.float32)
     for b in range(B):
         s = synth.old_scores(g, ld_s, ties=(b % 2 == 0))
@@ -261,11 +264,13 @@ def test_compact_matches_oracle_bytes(E, page):
     dsc = torch.full((B, ld_s), -9.0, device="cuda")
     dpos = torch.full((B, ld_s), -9, dtype=torch.int32, device="cuda")
     status = torch.zeros(B, dtype=torch.int32, device="cuda")
+    cws_n = E.compact_workspace_bytes(cfg)
+    cws = torch.zeros(cws_n, dtype=torch.uint8, device="cuda")
     E.epikv_compact(cfg, E.pool_of(src_t.view(L, 2, n_src, page, H, d)),
                     dev(src_pt), src_pt.shape[1],
                     E.pool_of(dst_t.view(L, 2, n_dst, page, H, d)),
                     dev(dst_pt), dst_pt.shape[1], dev(keep), dev(n_keep),
-                    dev(sc), dsc, dev(pos), dpos, ld_s, status)
+                    dev(sc), dsc, dev(pos), dpos, ld_s, status, cws, cws_n)
     _sync()
     dst = host(dst_t)
     dsc, dpos = host(dsc), host(dpos)
