@@ -1,0 +1,308 @@
+"""End-to-end parity of epikv_evict_step against the oracle.
+
+* A multi-step replay: one stream scored chunk by chunk with the state
+  carried on the GPU, the cache evicted to K whenever it overflows and
+  rebuilt into alternating page pools.  Per-step resync: each step's oracle
+  selection starts from the cache the GPU actually kept, so a near-tie that
+  went the other way cannot cascade.
+* A small ragged batch with prefill protection.
+* The batched step at its full size (32 sequences of 8k..32k tokens, K=4096,
+  32 layers) in the launch configuration the benchmark times, checked on
+  sampled sequences and rows.
+
+Scores within 1e-3 (relative, floor 1); retained positions exact when the
+oracle ranks the GPU's own fp32 scores, and equal to the oracle's fp64
+ranking except for positions whose oracle scores sit within 1e-3 of the
+cut; compacted rows bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from harness import dev, host, tie_exempt_compare
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def E():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26472_amd import epikv
+    epikv.lib()
+    return epikv
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+def _rel_err(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref))))
+
+
+def _oracle_stream_scores(hid_all, na, nb, w=64, eps=1e-6):
+    """Frozen fp64 scores of every token of one stream scored from its start
+    (hid_all: uint16 [n_band][T][D])."""
+    n_band = na + nb
+    T = hid_all.shape[1]
+    sm = np.zeros((n_band, T))
+    for l in range(n_band):
+        h = O.bf16_to_float64(hid_all[l])
+        g, has = O.residual_delta(h, None)
+        sm[l] = O.smooth_stream(np.zeros(0), g, has, O.SMOOTH_Z, w, eps)
+    return O.band_score(sm, na, nb)
+
+
+# ---------------------------------------------------------------------------
+# Multi-step replay of one stream
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name,steps,min_evict,row_sample", [
+    ("drift_replay", 16, 12, None), ("spike_replay", 40, 8, 256)])
+def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
+    import torch
+    w = synth.workload(name)
+    print(f"replay {name} steps={steps}", flush=True)
+    g = synth.rng(w.seed)
+    C, K, page = w.chunk, w.budget, w.page_size
+    L, H, d, D = w.n_layers, w.n_kv_heads, w.head_dim, w.hidden
+    na, nb = len(w.band_a), len(w.band_b)
+    T = C * steps
+    # the stream: hidden states of the band layers and every token's KV rows
+    a = synth.amplitudes(w, g, 0, T)
+    hid_all = np.empty((w.n_band, T, D), dtype=np.uint16)
+    for l in range(w.n_band):
+        hid_all[l] = synth.hidden_rows(a[l], D, g)
+    kv_tok = synth.random_bits16(g, (T, L, 2, H * d))
+    s_ref = _oracle_stream_scores(hid_all, na, nb, w.window)
+
+    cap = K + C                                  # most tokens ever cached
+    n_pages = (cap + page - 1) // page
+    cfg = E.default_cfg(batch=1, hidden=D, n_layers=L, n_band_a=na,
+                        n_band_b=nb, budget=K, page_size=page)
+    pools = [torch.zeros((L, 2, n_pages, page, H * d), dtype=torch.int16,
+                         device="cuda") for _ in range(2)]
+    pts = [dev(g.permutation(n_pages).astype(np.int32)[None, :])
+           for _ in range(2)]
+    pts_h = [host(p)[0] for p in pts]
+    scores = [torch.zeros((1, cap), device="cuda") for _ in range(2)]
+    pos = [torch.full((1, cap), -1, dtype=torch.int32, device="cuda")
+           for _ in range(2)]
+    states = [torch.zeros(E.state_bytes(cfg), dtype=torch.uint8,
+                          device="cuda") for _ in range(2)]
+    E.epikv_state_init(cfg, states[0])
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    keep = torch.zeros((1, K), dtype=torch.int32, device="cuda")
+    n_keep = torch.zeros(1, dtype=torch.int32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n_prefix = torch.zeros(1, dtype=torch.int32, device="cuda")
+    cache_tok = np.zeros(0, dtype=np.int64)     # token ids held, in order
+    x = 0                                        # pool holding the cache
+    R = O.default_recent(K)
+    evictions = swaps = 0
+    for step in range(steps):
+        t0 = step * C
+        new_tok = np.arange(t0, t0 + C)
+        n_prev = cache_tok.size
+        N = n_prev + C
+        # decode appends the chunk's KV rows, positions and (empty) scores
+        p = np.arange(n_prev, N)
+        pool_h = pools[x]
+        rows = dev(kv_tok[new_tok].transpose(1, 2, 0, 3))   # [L][2][C][HD]
+        pg = torch.from_numpy(pts_h[x][p // page].astype(np.int64)).cuda()
+        sl = torch.from_numpy((p % page).astype(np.int64)).cuda()
+        pool_h[:, :, pg, sl, :] = rows
+        pos[x][0, n_prev:N] = torch.from_numpy(new_tok.astype(np.int32)).cuda()
+        hid = dev(np.ascontiguousarray(hid_all[:, None, t0:t0 + C, :]))
+        io = E.make_step_io(
+            C, [hid[l] for l in range(w.n_band)], D, C * D,
+            dev(np.array([N], np.int32)), n_prefix,
+            E.pool_of(pools[x].view(L, 2, n_pages, page, H, d)), pts[x],
+            n_pages, E.pool_of(pools[1 - x].view(L, 2, n_pages, page, H, d)),
+            pts[1 - x], n_pages, scores[x], cap, states[0], states[1], keep,
+            n_keep, status, ws, ws_n, dst_scores=scores[1 - x],
+            src_pos=pos[x], dst_pos=pos[1 - x])
+        E.epikv_evict_step(cfg, io)
+        _sync()
+        assert host(status)[0] == 0
+        nk = int(host(n_keep)[0])
+        all_tok = np.concatenate([cache_tok, new_tok])
+        gpu_scores = host(scores[x])[0, :N]
+        # frozen scores of the new chunk
+        assert _rel_err(gpu_scores[n_prev:], s_ref[new_tok]) <= TOL, step
+        kidx = host(keep)[0, :nk]
+        # same-precision decision: the oracle ranking the GPU's fp32 scores
+        ref32 = O.select_keep(gpu_scores, 0, K, R)
+        assert np.array_equal(kidx, ref32), step
+        # against the oracle's own fp64 scores, with the near-tie exemption
+        ref64 = O.select_keep(s_ref[all_tok], 0, K, R)
+        if N > K:
+            swaps += tie_exempt_compare(kidx, ref64, s_ref[all_tok], 0, N,
+                                        K, R)
+        if N > K:
+            evictions += 1
+        # the rebuilt cache: token ids, scores and every row bit-exact
+        kept_tok = all_tok[kidx]
+        assert np.array_equal(host(pos[1 - x])[0, :nk], kept_tok)
+        assert np.array_equal(host(scores[1 - x])[0, :nk], gpu_scores[kidx])
+        j = np.arange(nk)
+        if row_sample is not None and nk > row_sample:
+            j = np.sort(g.choice(nk, row_sample, replace=False))
+        dst = host(pools[1 - x][:, :, torch.from_numpy(
+            pts_h[1 - x][j // page].astype(np.int64)).cuda(),
+            torch.from_numpy((j % page).astype(np.int64)).cuda(), :])
+        exp = O.compact_rows(kv_tok[all_tok], kidx[j])       # [n][L][2][HD]
+        assert np.array_equal(dst.transpose(2, 0, 1, 3), exp), step
+        cache_tok = kept_tok
+        x = 1 - x
+        states = [states[1], states[0]]
+    assert evictions >= min_evict
+    print(f"replay {name}: {evictions} evictions, {swaps} near-tie swaps",
+          flush=True)
+
+
+# ---------------------------------------------------------------------------
+# A small ragged batch with prefill protection and a budget error
+# ---------------------------------------------------------------------------
+def test_small_batch_matches_oracle(E):
+    import torch
+    print("small batch", flush=True)
+    g = synth.rng(700)
+    w = synth.workload("ragged_batch32", B=5, n_min=300, n_max=900,
+                       budget=256, chunk=64, n_layers=4)
+    C, K, page = w.chunk, w.budget, w.page_size
+    L, H, d, D = w.n_layers, w.n_kv_heads, w.head_dim, w.hidden
+    na, nb = len(w.band_a), len(w.band_b)
+    lengths = synth.ragged_lengths(w, g)
+    lengths[4] = 200                               # N <= K: keep all
+    prefix = np.array([0, 40, 0, 250, 0], np.int32)  # seq 3: P + R >= K
+    hid, before, _ = synth.hidden_chunk(w, g, lengths - C, C)
+    ring = synth.prior_samples(w, g, 63)
+    ld_s = int(lengths.max())
+    sc = np.zeros((w.B, ld_s), np.float32)
+    for b in range(w.B):
+        sc[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C,
+                                                  ties=True)
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.page_tables(np.full(w.B, K), page, g)
+    pool = synth.random_bits16(g, (L, 2, n_src, page, H * d))
+    cfg = E.default_cfg(batch=w.B, n_layers=L, budget=K)
+    st = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8)
+    sec = E.state_sections(cfg, st)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32))
+    sec["ring"][:] = torch.from_numpy(ring)
+    sec["h_prev"][:] = torch.from_numpy(before.transpose(1, 0, 2).copy()
+                                        .view(np.int16))
+    st_in = st.cuda()
+    st_out = torch.zeros_like(st_in)
+    hd = dev(hid)
+    src = dev(pool)
+    dstp = torch.full((L, 2, n_dst, page, H * d), 0x3C3C, dtype=torch.int16,
+                      device="cuda")
+    scores = dev(sc)
+    dsc = torch.zeros_like(scores)
+    keep = torch.full((w.B, K), -1, dtype=torch.int32, device="cuda")
+    n_keep = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+    status = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    io = E.make_step_io(
+        C, [hd[l] for l in range(w.n_band)], D, C * D,
+        dev(lengths.astype(np.int32)), dev(prefix),
+        E.pool_of(src.view(L, 2, n_src, page, H, d)), dev(src_pt),
+        src_pt.shape[1], E.pool_of(dstp.view(L, 2, n_dst, page, H, d)),
+        dev(dst_pt), dst_pt.shape[1], scores, ld_s, st_in, st_out, keep,
+        n_keep, status, ws, ws_n, dst_scores=dsc)
+    E.epikv_evict_step(cfg, io)
+    _sync()
+    gs, kh, nkh, sth = host(scores), host(keep), host(n_keep), host(status)
+    dst = host(dstp)
+    R = O.default_recent(K)
+    for b in range(w.B):
+        N = int(lengths[b])
+        prior = [ring[b, l].astype(np.float64) for l in range(w.n_band)]
+        s_new, *_ = O.hs_chunk_scores(
+            O.bf16_to_float64(hid[:, b]), O.bf16_to_float64(before[:, b]),
+            prior, na, nb)
+        assert _rel_err(gs[b, N - C:N], s_new) <= TOL, b
+        ref = O.select_keep(gs[b, :N], int(prefix[b]), K, R)
+        if isinstance(ref, str):
+            assert sth[b] == E.SEQ_BUDGET and nkh[b] == -1
+            assert np.all(dst[:, :, dst_pt[b, :K // page]] == 0x3C3C)
+            continue
+        assert sth[b] == 0 and nkh[b] == ref.size
+        assert np.array_equal(kh[b, :ref.size], ref)
+        s64 = np.concatenate([sc[b, :N - C].astype(np.float64), s_new])
+        ref64 = O.select_keep(s64, int(prefix[b]), K, R)
+        if N > K:
+            tie_exempt_compare(kh[b, :ref.size], ref64, s64, int(prefix[b]),
+                               N, K, R)
+        n = ref.size
+        pos = np.arange(N)
+        src_rows = pool[:, :, src_pt[b, pos // page], pos % page]
+        exp = O.compact_rows(src_rows.transpose(2, 0, 1, 3), ref)
+        j = np.arange(n)
+        got = dst[:, :, dst_pt[b, j // page], j % page].transpose(2, 0, 1, 3)
+        assert np.array_equal(got, exp), b
+        assert np.array_equal(host(dsc)[b, :n], gs[b, ref])
+
+
+# ---------------------------------------------------------------------------
+# The batched step at full size, launch configuration of the benchmark
+# ---------------------------------------------------------------------------
+def test_full_size_batched_step_sampled(E):
+    import torch
+    import bench
+    print("full-size batched step", flush=True)
+    w = synth.workload("ragged_batch32")
+    S = bench.setup_hs(w, E)
+    E.epikv_evict_step(S.cfg, S.io)
+    _sync()
+    keep1 = host(S.keep_idx).copy()
+    gs = host(S.scores)
+    st = host(S.status)
+    nk = host(S.n_keep)
+    assert np.all(st == 0) and np.all(nk == w.budget)
+    # determinism: a second identical step gives identical bits
+    dst_sample = host(S.dst_pool[:, :, :64]).copy()
+    out_state = host(S.state_out).copy()
+    E.epikv_evict_step(S.cfg, S.io)
+    _sync()
+    assert np.array_equal(host(S.keep_idx), keep1)
+    assert np.array_equal(host(S.dst_pool[:, :, :64]), dst_sample)
+    assert np.array_equal(host(S.state_out), out_state)
+
+    C, K, page = w.chunk, w.budget, w.page_size
+    na, nb = len(w.band_a), len(w.band_b)
+    R = O.default_recent(K)
+    g = synth.rng(901)
+    for b in [0, 7, 19, 31]:
+        N = int(S.lengths[b])
+        prior = [S.ring_host[b, l].astype(np.float64) for l in range(w.n_band)]
+        s_new, *_ = O.hs_chunk_scores(
+            O.bf16_to_float64(S.hidden_host[:, b]),
+            O.bf16_to_float64(S.before_host[:, b]), prior, na, nb)
+        assert _rel_err(gs[b, N - C:N], s_new) <= TOL, b
+        ref = O.select_keep(gs[b, :N], 0, K, R)
+        assert np.array_equal(keep1[b], ref), b
+        s64 = np.concatenate([S.old_scores[b].astype(np.float64), s_new])
+        tie_exempt_compare(keep1[b], O.select_keep(s64, 0, K, R), s64, 0, N,
+                           K, R)
+        # sampled rows of the rebuilt cache, every layer and K/V
+        js = np.sort(g.choice(K, 48, replace=False))
+        src_rows = host(S.src_pool[:, :, torch.from_numpy(
+            S.src_pt_host[b, ref[js] // page].astype(np.int64)).cuda(),
+            torch.from_numpy((ref[js] % page).astype(np.int64)).cuda(), :])
+        dst_rows = host(S.dst_pool[:, :, torch.from_numpy(
+            S.dst_pt_host[b, js // page].astype(np.int64)).cuda(),
+            torch.from_numpy((js % page).astype(np.int64)).cuda(), :])
+        assert np.array_equal(src_rows, dst_rows), b
+        assert np.array_equal(host(S.dst_scores)[b, :K], gs[b, ref])
+        assert np.array_equal(host(S.dst_pos)[b, :K], ref.astype(np.int32))
