@@ -512,8 +512,10 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   if (st) return st;
   char* ws = (char*)io->workspace;
   char* ws_offsets = ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk);
+  // The scores are compacted only when the caller asks for them.
+  const float* src_scores = io->dst_scores ? io->scores : nullptr;
   st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
-                     io->keep_idx, io->n_keep, io->scores, io->dst_scores, io->src_pos, io->dst_pos,
+                     io->keep_idx, io->n_keep, src_scores, io->dst_scores, io->src_pos, io->dst_pos,
                      io->ld_s, ws_offsets, compact_ws_bytes(cfg));
   if (st) return st;
   const size_t ws_state = state_layout(cfg).total;
@@ -534,10 +536,9 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                                           io->keep_idx, io->n_keep, io->seq_status, io->chunk),
                               stream));
   if (st) return st;
-  const bool with_scores = io->dst_scores != nullptr;
   return launched(launch_compact(
       compact_args(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
-                   io->keep_idx, io->n_keep, with_scores ? io->scores : nullptr, io->dst_scores,
+                   io->keep_idx, io->n_keep, src_scores, io->dst_scores,
                    io->src_pos, io->dst_pos, io->ld_s, io->seq_status, ws_offsets),
       stream));
 }

@@ -104,10 +104,26 @@ def test_strerror_covers_every_code(E):
 
 
 # Fake device addresses: aligned, never dereferenced (every call below fails
-# validation on the host).
+# validation on the host).  On a machine with a GPU these calls are skipped:
+# a validation bug there would launch a kernel on addresses that do not
+# exist.
 A = 1 << 20
 
 
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:
+        return True
+
+
+host_only = pytest.mark.skipif(not _no_gpu(),
+                               reason="fake-pointer validation runs only "
+                                      "without a GPU")
+
+
+@host_only
 def test_score_validation(E):
     L = E.lib()
     c = E.default_cfg(batch=2, n_band_a=1, n_band_b=1)
@@ -151,6 +167,7 @@ def test_score_validation(E):
              A, A, 8 * A, 3 * A, 9 * A, 1 << 30, None) == E.EPIKV_EINVAL_SHAPE
 
 
+@host_only
 def test_zscore_select_compact_validation(E):
     L = E.lib()
     c = E.default_cfg(batch=2, budget=256)
@@ -198,6 +215,7 @@ def test_zscore_select_compact_validation(E):
               None) == E.EPIKV_EALIAS
 
 
+@host_only
 def test_evict_step_validation(E):
     L = E.lib()
     c = E.default_cfg(batch=2, budget=256)
@@ -217,3 +235,49 @@ def test_evict_step_validation(E):
     io.chunk = 0
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EINVAL_SHAPE
+
+
+def _valid_io(E, A):
+    """A step description whose pointers are aligned fake addresses."""
+    io = E.StepIO()
+    io.chunk = 64
+    hid = (ctypes.c_void_p * 15)(*[A * (i + 2) for i in range(15)])
+    io._keep = hid
+    io.hidden = ctypes.cast(hid, ctypes.POINTER(ctypes.c_void_p))
+    io.ld_tok, io.ld_seq = 4096, 64 * 4096
+    io.n_cached = io.n_prefix = A
+    io.src = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
+    io.dst = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
+    io.src_pt = io.dst_pt = A
+    io.ld_src_pt, io.ld_dst_pt = 64, 16
+    io.scores = 64 * A
+    io.ld_s = 1024
+    io.state_in, io.state_out = 128 * A, 256 * A
+    io.keep_idx = io.n_keep = io.seq_status = A
+    io.workspace = 512 * A
+    io.workspace_bytes = 1 << 30
+    return io
+
+
+@host_only
+def test_evict_step_scores_copy_is_optional(E):
+    """Without dst_scores the step must not demand a score pair; the first
+    error it finds in this description is the missing n_prefix."""
+    L = E.lib()
+    c = E.default_cfg(batch=2, budget=256)
+    io = _valid_io(E, A)
+    io.n_prefix = None
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_NULL
+    io = _valid_io(E, A)
+    io.dst_pos = A                       # positions on one side only
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_NULL
+    io = _valid_io(E, A)
+    io.state_out = io.state_in           # state must not be updated in place
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS
+    io = _valid_io(E, A)
+    io.workspace = io.state_in           # workspace overlapping the state
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS
