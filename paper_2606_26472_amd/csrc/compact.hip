@@ -9,12 +9,13 @@
 //            into the byte offsets of the source and destination rows inside
 //            a plane (one 16-byte record per slot, in the workspace), and
 //            copies the slot's score and position;
-//   gather   a 256-thread workgroup owns rows_per_block consecutive slots of
-//            one sequence for lk_per_block planes.  Each thread loads the
-//            offset record of its row and then streams its NV 16-byte
-//            columns of every plane: one dependent load before the data,
-//            so short-lived workgroups keep HBM busy.  Loads and stores are
-//            non-temporal: each byte is touched once.
+//   gather   a 256-thread workgroup owns four consecutive slots of one
+//            sequence (one wavefront per slot) for lk_per_block planes.  The
+//            wavefront reads its slot's offset record with a scalar load and
+//            then streams the row's 16-byte columns of every plane: a single
+//            dependent load before the data, so short-lived workgroups keep
+//            HBM busy.  Loads and stores are non-temporal: each byte is
+//            touched once.
 #include "epikv_internal.h"
 
 namespace epikv {
@@ -61,39 +62,23 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_resolve(CompactArgs
   }
 }
 
+// One wavefront per destination row: the row's offset record, n_keep and
+// the plane bases are wave-uniform (scalar loads), lane l streams the
+// row's 16-byte columns l, l+64, ... (NV of them) of each plane.
 template <int NV, int PL>
 __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
-  const int tid = threadIdx.x;
-  const int b = blockIdx.x / a.blocks_per_seq;
-  const int cb = blockIdx.x - b * a.blocks_per_seq;
-  const int j0 = cb * a.rows_per_block;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int b = blockIdx.z;
+  const int j = blockIdx.x * kCompactWaves + wave;
   const int row_vec = a.row_bytes >> 4;
-  // The offset records of slots < K are always readable, so they are loaded
-  // alongside n_keep rather than after it.
-  int64_t so[NV];
-  int64_t dof[NV];
-  int jr[NV];
-#pragma unroll
-  for (int q = 0; q < NV; ++q) {
-    const int v = tid + q * kCompactThreads;
-    const int r = v / row_vec;
-    const int j = j0 + r;
-    jr[q] = (r < a.rows_per_block && j < a.K) ? j : -1;
-    so[q] = -1;
-    dof[q] = 0;
-    if (jr[q] >= 0) {
-      const int64_t col = (int64_t)(v - r * row_vec) * 16;
-      const u32x4 rec = *reinterpret_cast<const u32x4*>(a.offsets + 2 * ((int64_t)b * a.K + j));
-      const int64_t s0 = (int64_t)(((uint64_t)rec[1] << 32) | rec[0]);
-      const int64_t d0 = (int64_t)(((uint64_t)rec[3] << 32) | rec[2]);
-      so[q] = s0 >= 0 ? s0 + col : -1;
-      dof[q] = d0 + col;
-    }
-  }
+  // The record of slot min(j, K-1) is always readable, so it is fetched
+  // together with n_keep instead of after it.
+  const int64_t* rec = a.offsets + 2 * ((int64_t)b * a.K + min(j, a.K - 1));
+  const int64_t s0 = rec[0];
+  const int64_t d0 = rec[1];
   const int nk = min(a.n_keep[b], a.K);
-#pragma unroll
-  for (int q = 0; q < NV; ++q)
-    if (jr[q] >= nk) so[q] = -1;
+  if (j >= nk || s0 < 0) return;
 
   const int lk0 = blockIdx.y * a.lk_per_block;
   const int lk1 = min(a.n_lk, lk0 + a.lk_per_block);
@@ -103,20 +88,24 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
     for (int p = 0; p < PL; ++p) {
       const int pl = lk + p;
       if (pl < lk1) {
-        const char* sb = a.src + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv;
+        const char* sb = a.src + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + s0;
 #pragma unroll
-        for (int q = 0; q < NV; ++q)
-          if (so[q] >= 0) val[p][q] = ld_stream(sb + so[q]);
+        for (int q = 0; q < NV; ++q) {
+          const int c = lane + q * 64;
+          if (c < row_vec) val[p][q] = ld_stream(sb + (int64_t)c * 16);
+        }
       }
     }
 #pragma unroll
     for (int p = 0; p < PL; ++p) {
       const int pl = lk + p;
       if (pl < lk1) {
-        char* db = a.dst + (int64_t)(pl >> 1) * a.d_layer + (int64_t)(pl & 1) * a.d_kv;
+        char* db = a.dst + (int64_t)(pl >> 1) * a.d_layer + (int64_t)(pl & 1) * a.d_kv + d0;
 #pragma unroll
-        for (int q = 0; q < NV; ++q)
-          if (so[q] >= 0) st_stream(db + dof[q], val[p][q]);
+        for (int q = 0; q < NV; ++q) {
+          const int c = lane + q * 64;
+          if (c < row_vec) st_stream(db + (int64_t)c * 16, val[p][q]);
+        }
       }
     }
   }
@@ -124,20 +113,17 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
 
 template <int NV, int PL>
 hipError_t launch(const CompactArgs& a, hipStream_t s) {
-  dim3 grid(a.B * a.blocks_per_seq, (a.n_lk + a.lk_per_block - 1) / a.lk_per_block);
+  dim3 grid(a.blocks_per_seq, (a.n_lk + a.lk_per_block - 1) / a.lk_per_block, a.B);
   hipLaunchKernelGGL((k_compact<NV, PL>), grid, dim3(kCompactThreads), 0, s, a);
   return hipGetLastError();
 }
 
 template <int PL>
 hipError_t launch_nv(const CompactArgs& a, hipStream_t s) {
-  const int tile_vec = a.rows_per_block * (a.row_bytes >> 4);
-  const int nv = (tile_vec + kCompactThreads - 1) / kCompactThreads;
-  if (nv <= 1) return launch<1, PL>(a, s);
-  if (nv <= 2) return launch<2, PL>(a, s);
-  if (nv <= 4) return launch<4, PL>(a, s);
-  if (nv <= 8) return launch<8, PL>(a, s);
-  if (nv <= 16) return launch<16, PL>(a, s);
+  const int row_vec = a.row_bytes >> 4;
+  if (row_vec <= 64) return launch<1, PL>(a, s);
+  if (row_vec <= 128) return launch<2, PL>(a, s);
+  if (row_vec <= 256) return launch<4, PL>(a, s);
   return hipErrorInvalidValue;
 }
 

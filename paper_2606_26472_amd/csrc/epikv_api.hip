@@ -85,9 +85,8 @@ int check_cfg(const epikv_cfg* c) {
   const int hd = c->n_kv_heads * c->head_dim;
   if (hd > 2048) return EPIKV_EINVAL_SHAPE;
   const int row_vec = hd / 8;
-  // One row of one plane must fit the per-thread column budget of a
-  // compaction workgroup.
-  if (row_vec > kCompactThreads * kCompactMaxVec) return EPIKV_EINVAL_SHAPE;
+  // One row of one plane is streamed by one wavefront (at most 4 16-byte
+  // columns per lane): H*d <= 2048 guarantees it.
   if (c->signal == EPIKV_SIGNAL_LAGKV && (kScoreThreads % row_vec) != 0) return EPIKV_EINVAL_SHAPE;
   if (c->signal == EPIKV_SIGNAL_HS) {
     if (c->n_band_a < 1 || c->n_band_b < 0 || n_band(c) > EPIKV_MAX_BAND) return EPIKV_EINVAL_SHAPE;
@@ -336,18 +335,12 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.page_size = c->page_size;
   a.row_bytes = row_bytes(c);
   a.n_lk = 2 * c->n_layers;
-  // Tile: about 8 KiB of row data per plane (two 16-byte vectors per
-  // thread), at least one row, one plane per workgroup; measured best among
-  // 2..16 rows x 1..64 planes for 32 sequences
-  // keeping 4096 of 8k..32k tokens.
-  const int row_vec = row_bytes(c) / 16;
-  int rows = 2 * kCompactThreads / row_vec;
-  if (rows < 1) rows = 1;
-  if (rows > kCompactMaxRows) rows = kCompactMaxRows;
-  a.rows_per_block = rows;
+  // One wavefront per destination row, four rows and one (layer, K|V)
+  // plane per workgroup: measured best on MI355X among 2..16 rows x 1..64
+  // planes for 32 sequences keeping 4096 of 8k..32k tokens.
   a.lk_per_block = 1;
   a.planes_together = 1;
-  a.blocks_per_seq = (c->budget + rows - 1) / rows;
+  a.blocks_per_seq = (c->budget + kCompactWaves - 1) / kCompactWaves;
   return a;
 }
 

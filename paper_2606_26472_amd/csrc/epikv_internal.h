@@ -108,10 +108,9 @@ struct CompactArgs {
   int32_t* seq_status;                     // optional
   int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
   int32_t B, K, page_size, row_bytes, n_lk;
-  int32_t rows_per_block;                  // destination slots per workgroup
   int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
   int32_t planes_together;                 // planes loaded before storing (1,2,4,8)
-  int32_t blocks_per_seq;                  // ceil(K / rows_per_block)
+  int32_t blocks_per_seq;                  // ceil(K / kCompactWaves)
 };
 
 struct FillArgs {
@@ -138,8 +137,7 @@ constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
-constexpr int kCompactMaxVec = 16;       // 16-byte vectors per thread per (layer, K|V)
-constexpr int kCompactMaxRows = 256;     // destination slots per compact workgroup
+constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per gather workgroup
 constexpr int kLagMaxLds = 48 * 1024;
 
 }  // namespace epikv
