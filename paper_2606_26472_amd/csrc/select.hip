@@ -12,13 +12,15 @@
 //      atomics), a block-wide suffix scan finds the digit holding the M-th
 //      key.  After three passes the threshold T is exact and `need` says
 //      how many keys equal to T are kept;
-//   2. one ordered sweep over the positions in tiles of 1024: a ballot
-//      prefix count ranks the keys equal to T by position (the first `need`
-//      of them are kept) and a second one gives every kept position its
-//      output slot, so keep_idx comes out ascending without a sort.
-// For N up to 64 Ki positions every thread keeps the keys of its positions
-// (tid, tid+1024, ...) in registers for all four sweeps; longer sequences
-// re-read the scores from global memory (L2) in each sweep.
+//   2. the kept positions in order: keys equal to T are ranked by position
+//      with a prefix count (the first `need` of them are kept) and a second
+//      prefix count gives every kept position its output slot, so keep_idx
+//      comes out ascending without a sort.
+// For N up to 32 Ki positions thread t keeps the keys of the contiguous
+// positions [t*KPT, (t+1)*KPT) in registers for all four sweeps, so step 2
+// needs two workgroup-wide scans in total.  Longer sequences re-read the
+// scores from global memory (L2) in each sweep and produce the output in
+// tiles of 1024 positions.
 #include "epikv_internal.h"
 
 namespace epikv {
@@ -71,7 +73,32 @@ __device__ __forceinline__ uint32_t block_flag_rank(bool flag, uint32_t* wsum, u
   return pre + below;
 }
 
-// KPT > 0: positions tid + k*1024 (k < KPT) have their keys in registers.
+// Exclusive prefix over the workgroup in thread order, and the total.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
+                                                         uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t t = __shfl_up(x, off, 64);
+    if (lane >= off) x += t;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  uint32_t pre = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t y = wsum[w];
+    pre += (w < wave) ? y : 0u;
+    tot += y;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + x - v;
+}
+
+// KPT > 0: positions [tid*KPT, (tid+1)*KPT) have their keys in registers.
 // KPT == 0: keys are recomputed from global memory in every sweep.
 template <int KPT>
 __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
@@ -113,10 +140,11 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
   const int lo = P, hi = N - R;  // eligible positions [lo, hi)
   constexpr int KR = KPT > 0 ? KPT : 1;
   uint32_t keys[KR];
+  const int base = tid * KR;  // first position owned (register path)
   if (KPT > 0) {
 #pragma unroll
     for (int k = 0; k < KR; ++k) {
-      const int i = tid + k * kSelectThreads;
+      const int i = base + k;
       keys[k] = (i >= lo && i < hi) ? rank_key(s[i]) : 0u;
     }
   }
@@ -135,7 +163,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
     if (KPT > 0) {
 #pragma unroll
       for (int k = 0; k < KR; ++k) {
-        const int i = tid + k * kSelectThreads;
+        const int i = base + k;
         if (i >= lo && i < hi && (keys[k] & mask) == prefix)
           atomicAdd(&hist[(keys[k] >> shift) & dmask], 1u);
       }
@@ -177,34 +205,63 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
 
   // need = keys equal to T that are kept, lowest positions first.
   const uint32_t T = prefix;
-  uint32_t eq_seen = 0u, written = 0u;
-  const int tiles = (N + kSelectThreads - 1) / kSelectThreads;
-#pragma unroll 1
-  for (int t = 0; t < tiles; ++t) {
-    const int i = t * kSelectThreads + tid;
-    const bool valid = i < N;
-    const bool prot = valid && (i < lo || i >= hi);
-    const bool elig = valid && !prot;
-    uint32_t key = 0u;
-    if (elig) {
-      if (KPT > 0) {
+  uint32_t written = 0u;
+  if (KPT > 0) {
+    uint32_t n_eq = 0u;
 #pragma unroll
-        for (int k = 0; k < KR; ++k)
-          if (k == t) key = keys[k];
-      } else {
-        key = rank_key(s[i]);
+    for (int k = 0; k < KR; ++k) {
+      const int i = base + k;
+      n_eq += (i >= lo && i < hi && keys[k] == T) ? 1u : 0u;
+    }
+    uint32_t eq_tot;
+    uint32_t eq_rank = block_exclusive_scan(n_eq, wsum, &eq_tot);
+    uint64_t keep_bits = 0ull;
+    uint32_t n_keep_t = 0u;
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+      const int i = base + k;
+      if (i < N) {
+        const bool elig = i >= lo && i < hi;
+        bool keep = !elig || keys[k] > T;
+        if (elig && keys[k] == T) {
+          keep = eq_rank < need;
+          ++eq_rank;
+        }
+        if (keep) {
+          keep_bits |= 1ull << k;
+          ++n_keep_t;
+        }
       }
     }
-    const bool gt = elig && key > T;
-    const bool eq = elig && key == T;
-    uint32_t eq_tot;
-    const uint32_t eq_rank = eq_seen + block_flag_rank(eq, wsum, &eq_tot);
-    const bool keep = prot || gt || (eq && eq_rank < need);
-    uint32_t keep_tot;
-    const uint32_t slot = written + block_flag_rank(keep, wsum, &keep_tot);
-    if (keep && slot < (uint32_t)K) out[slot] = i;
-    eq_seen += eq_tot;
-    written += keep_tot;
+    uint32_t slot = block_exclusive_scan(n_keep_t, wsum, &written);
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+      if ((keep_bits >> k) & 1ull) {
+        if (slot < (uint32_t)K) out[slot] = base + k;
+        ++slot;
+      }
+    }
+  } else {
+    uint32_t eq_seen = 0u;
+    const int tiles = (N + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+    for (int t = 0; t < tiles; ++t) {
+      const int i = t * kSelectThreads + tid;
+      const bool valid = i < N;
+      const bool prot = valid && (i < lo || i >= hi);
+      const bool elig = valid && !prot;
+      const uint32_t key = elig ? rank_key(s[i]) : 0u;
+      const bool gt = elig && key > T;
+      const bool eq = elig && key == T;
+      uint32_t eq_tot;
+      const uint32_t eq_rank = eq_seen + block_flag_rank(eq, wsum, &eq_tot);
+      const bool keep = prot || gt || (eq && eq_rank < need);
+      uint32_t keep_tot;
+      const uint32_t slot = written + block_flag_rank(keep, wsum, &keep_tot);
+      if (keep && slot < (uint32_t)K) out[slot] = i;
+      eq_seen += eq_tot;
+      written += keep_tot;
+    }
   }
   if (tid == 0) {
     const bool ok = written == (uint32_t)K;
@@ -223,7 +280,8 @@ hipError_t launch(const SelectArgs& a, hipStream_t s) {
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
   // Registers per thread for the keys: the smallest power of two covering
-  // ld_s positions (every N is at most ld_s).
+  // ld_s positions (every N is at most ld_s); beyond 32 per thread the keys
+  // would spill, so longer rows take the global-memory variant.
   const int64_t per = (a.ld_s + kSelectThreads - 1) / kSelectThreads;
   if (per <= 1) return launch<1>(a, s);
   if (per <= 2) return launch<2>(a, s);
@@ -231,7 +289,6 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
   if (per <= 8) return launch<8>(a, s);
   if (per <= 16) return launch<16>(a, s);
   if (per <= 32) return launch<32>(a, s);
-  if (per <= 64) return launch<64>(a, s);
   return launch<0>(a, s);
 }
 
