@@ -64,8 +64,11 @@ typedef enum epikv_seq_status {
 
 /* Which per-token signal is scored. */
 typedef enum epikv_signal {
-  EPIKV_SIGNAL_HS = 0,      /* band-layer hidden-state change, Sec. 3.2 Eq. 1 */
-  EPIKV_SIGNAL_LAGKV = 1    /* lag-normalised key+value variance, Sec. 3.3 */
+  EPIKV_SIGNAL_HS = 0,        /* band-layer hidden-state change, Sec. 3.2 Eq. 1 */
+  EPIKV_SIGNAL_LAGKV = 1,     /* lag-normalised key + value variance, Sec. 3.3 */
+  EPIKV_SIGNAL_KV_KEY = 2,    /* variance of the key vectors, Sec. 3.3 (KV-key) */
+  EPIKV_SIGNAL_KV_VAL = 3,    /* variance of the value vectors, Sec. 3.3 (KV-val) */
+  EPIKV_SIGNAL_LAGKV_KEY = 4  /* lag-normalised key variance (lag-kv-key, App. B) */
 } epikv_signal;
 
 /* How the per-token signal is smoothed over the trailing window. */
@@ -85,8 +88,8 @@ typedef enum epikv_smoothing {
  * (positive weight) first.  The paper's bands are layers 7..13 (A) and
  * 18..25 (B) of a 32-layer model (Sec. 3.2, App. A); the single-layer
  * preset A = {10}, B = {21} gives Eq. 3's z_10 - z_21.  n_band_b may be 0.
- * Lag-KV signal: one signal row per sequence, weight +1; the band fields
- * are ignored.
+ * KV-vector signals (Lag-KV, KV-key, KV-val, lag-kv-key): one signal row per
+ * sequence, weight +1; the band fields are ignored.
  */
 typedef struct epikv_cfg {
   int32_t batch;        /* B >= 1 sequences */
@@ -142,12 +145,14 @@ int epikv_check_cfg(const epikv_cfg* cfg);
  *                                 right-aligned (slot w-2 newest), unused
  *                                 slots 0
  *   [2] bf16  h_prev[B][n_band][D] HS: hidden state of the last token
- *   [3] float range[2][B][L][2][H][d] Lag-KV: per-channel min (first half)
- *                                 and max of the previous chunk
- * n_sig = n_band_a + n_band_b for HS, 1 for Lag-KV.  An HS stream yields a
- * sample for every token but its first (which has no predecessor); a
- * Lag-KV stream for every token.  Sections a signal does not use have size
- * 0.  Returns the total size in bytes, or 0 for an invalid cfg.
+ *   [3] float range[2][B][L][2][H][d] lag-normalised signals: per-channel
+ *                                 min (first half) and max of the previous
+ *                                 chunk
+ * n_sig = n_band_a + n_band_b for HS, 1 for the KV-vector signals.  An HS
+ * stream yields a sample for every token but its first (which has no
+ * predecessor); a KV-vector stream for every token.  Sections a signal does
+ * not use have size 0.  Returns the total size in bytes, or 0 for an invalid
+ * cfg.
  */
 size_t epikv_state_bytes(const epikv_cfg* cfg);
 
@@ -181,17 +186,20 @@ int epikv_state_init(const epikv_cfg* cfg, void* state, hipStream_t stream);
  *               16-byte aligned, ld_tok and ld_seq multiples of 8, rows of
  *               D elements.
  *   pool, page_table, ld_pt, n_cached   unused (may be NULL / 0).
- * Lag-KV signal (Sec. 3.3): the chunk's tokens are positions
- * [n_cached[b] - chunk, n_cached[b]) of the paged cache (page_table
- * int32 [B][ld_pt]).  Each channel of the token's key and value rows is
- * normalised by the previous chunk's per-channel range from state_in
- * (x - mn) / (mx - mn + eps) (the first chunk of a stream uses its own
- * range), the population variance over the head dimension is taken for K
- * and V and summed, and the sum is averaged over layers and KV heads:
- * sig[0][b][c].  hidden may be NULL.  Needs
- * epikv_workspace_bytes(cfg, chunk) bytes of workspace (ignored for HS).
+ * KV-vector signals (Sec. 3.3, Table 1): the chunk's tokens are positions
+ * [n_cached[b] - chunk, n_cached[b]) of the paged cache (page_table int32
+ * [B][ld_pt]).  For each used tensor (keys for KV-key and lag-kv-key, values
+ * for KV-val, both for Lag-KV) the population variance over the head
+ * dimension is taken per (layer, KV head) -- of the raw vectors, or for the
+ * lag-normalised signals of (x - mn) / (mx - mn + eps) with (mn, mx) the
+ * previous chunk's per-channel range from state_in (the first chunk of a
+ * stream uses its own range) -- the used tensors' variances are summed and
+ * averaged over layers and KV heads: sig[0][b][c].  hidden may be NULL.
+ * Needs epikv_workspace_bytes(cfg, chunk) bytes of workspace (ignored for
+ * HS).
  *
- * state_out receives h_prev (HS) or this chunk's range (Lag-KV); its
+ * state_out receives h_prev (HS) or this chunk's range (lag-normalised
+ * signals); its
  * counters and ring are written by epikv_zscore, so a step is complete only
  * after both calls.  state_in and state_out must not overlap.
  * sig: float [n_sig][B][chunk].
@@ -212,8 +220,8 @@ int epikv_score(const epikv_cfg* cfg, int32_t chunk,
  * state_in.ring; each token's window is the last min(w, available) samples
  * up to and including its own.  Z: (x - mu) / (sigma + eps) with the
  * population sigma; MEAN: mu; RAW: x.  Tokens without a sample get 0.  The
- * frozen score s = mean over Band A rows - mean over Band B rows (Lag-KV:
- * the single row) is written to scores[b*ld_s + n_cached[b] - chunk + c].
+ * frozen score s = mean over Band A rows - mean over Band B rows (KV-vector
+ * signals: the single row) is written to scores[b*ld_s + n_cached[b] - chunk + c].
  * Sequences with n_cached < chunk or n_cached > ld_s are skipped.
  *   sig       float [n_sig][B][chunk] from epikv_score.
  *   smoothed  optional (may be NULL) float [n_sig][B][chunk]: per-row

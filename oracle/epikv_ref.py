@@ -244,6 +244,43 @@ def lagkv_signal(k, v, mn, mx, eps=EPS_DEFAULT):
     return np.mean(var_k + var_v, axis=(1, 2))
 
 
+def kv_variance_signal(k, v, use_k=True, use_v=True, rng=None,
+                       eps=EPS_DEFAULT):
+    """Per-token signal of the KV-vector family (Sec. 3.3, Table 1).
+
+    For each used tensor (keys, values) the population variance over the
+    head dimension is taken per (token, layer, head) -- of the raw vectors
+    for KV-key / KV-val, of the vectors min-max normalised by `rng`
+    (= (mn, mx) of the previous chunk) for the lag-normalised variants; the
+    variances of the used tensors are summed and averaged over (layer,
+    head).  Lag-KV = keys + values normalised; lag-kv-key = keys only
+    (Tables B1-B4).
+    """
+    q = np.zeros(k.shape[0])
+    for use, x, kv in ((use_k, k, 0), (use_v, v, 1)):
+        if not use:
+            continue
+        if rng is not None:
+            mn, mx = rng
+            x = (x - mn[None, :, kv]) / (mx[None, :, kv] - mn[None, :, kv] + eps)
+        q = q + np.mean(np.var(x, axis=-1), axis=(1, 2))
+    return q
+
+
+def kv_chunk_scores(k, v, use_k, use_v, lag, prev_range, prior,
+                    mode=SMOOTH_MEAN, w=WINDOW_DEFAULT, eps=EPS_DEFAULT):
+    """Frozen scores of one chunk for any KV-vector signal; with lag=True the
+    previous chunk's range normalises (the first chunk uses its own, R14).
+    Returns (s, q, this chunk's (mn, mx))."""
+    own = chunk_range(k, v)
+    rng = None
+    if lag:
+        rng = own if prev_range is None else prev_range
+    q = kv_variance_signal(k, v, use_k, use_v, rng, eps)
+    s = smooth_stream(prior, q, np.ones(q.size, dtype=bool), mode, w, eps)
+    return s, q, own
+
+
 def lagkv_chunk_scores(k, v, prev_range, prior, mode=SMOOTH_MEAN,
                        w=WINDOW_DEFAULT, eps=EPS_DEFAULT):
     """Frozen Lag-KV scores of one chunk of new tokens.

@@ -24,6 +24,12 @@ int n_band(const epikv_cfg* c) { return c->n_band_a + c->n_band_b; }
 
 int n_sig(const epikv_cfg* c) { return c->signal == EPIKV_SIGNAL_HS ? n_band(c) : 1; }
 
+bool is_kv(int signal) { return signal != EPIKV_SIGNAL_HS; }
+
+bool uses_range(int signal) {
+  return signal == EPIKV_SIGNAL_LAGKV || signal == EPIKV_SIGNAL_LAGKV_KEY;
+}
+
 int recent_of(const epikv_cfg* c) {
   return c->recent >= 0 ? c->recent : (c->budget / 4 < 128 ? c->budget / 4 : 128);
 }
@@ -44,7 +50,7 @@ Layout state_layout(const epikv_cfg* c) {
   L.size[0] = 4 * B;
   L.size[1] = 4 * B * (size_t)n_sig(c) * (size_t)(c->window - 1);
   L.size[2] = c->signal == EPIKV_SIGNAL_HS ? 2 * B * (size_t)n_band(c) * (size_t)c->hidden : 0;
-  L.size[3] = c->signal == EPIKV_SIGNAL_LAGKV
+  L.size[3] = uses_range(c->signal)
                   ? 4 * 2 * B * (size_t)c->n_layers * 2 * (size_t)c->n_kv_heads * (size_t)c->head_dim
                   : 0;
   size_t o = 0;
@@ -65,13 +71,13 @@ size_t compact_ws_bytes(const epikv_cfg* c) {
 }
 
 size_t partial_bytes(const epikv_cfg* c, int chunk) {
-  if (c->signal != EPIKV_SIGNAL_LAGKV) return 0;
+  if (!is_kv(c->signal)) return 0;
   return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk);
 }
 
 int check_cfg(const epikv_cfg* c) {
   if (!c) return EPIKV_EINVAL_NULL;
-  if (c->signal != EPIKV_SIGNAL_HS && c->signal != EPIKV_SIGNAL_LAGKV) return EPIKV_EINVAL_PARAM;
+  if (c->signal < EPIKV_SIGNAL_HS || c->signal > EPIKV_SIGNAL_LAGKV_KEY) return EPIKV_EINVAL_PARAM;
   if (c->smoothing < EPIKV_SMOOTH_Z || c->smoothing > EPIKV_SMOOTH_RAW) return EPIKV_EINVAL_PARAM;
   if (c->window < 1 || c->window > EPIKV_MAX_WINDOW) return EPIKV_EINVAL_PARAM;
   if (!(c->eps >= 0.f) || !isfinite(c->eps)) return EPIKV_EINVAL_PARAM;
@@ -87,7 +93,7 @@ int check_cfg(const epikv_cfg* c) {
   const int row_vec = hd / 8;
   // One row of one plane is streamed by one wavefront (at most 4 16-byte
   // columns per lane): H*d <= 2048 guarantees it.
-  if (c->signal == EPIKV_SIGNAL_LAGKV && (kScoreThreads % row_vec) != 0) return EPIKV_EINVAL_SHAPE;
+  if (is_kv(c->signal) && (kScoreThreads % row_vec) != 0) return EPIKV_EINVAL_SHAPE;
   if (c->signal == EPIKV_SIGNAL_HS) {
     if (c->n_band_a < 1 || c->n_band_b < 0 || n_band(c) > EPIKV_MAX_BAND) return EPIKV_EINVAL_SHAPE;
     if (c->hidden < 8 || c->hidden > 16384 || (c->hidden % 8) != 0) return EPIKV_EINVAL_SHAPE;
@@ -186,6 +192,9 @@ void lag_args(const epikv_cfg* c, int32_t chunk, const epikv_pool* pool, const i
   a->H = c->n_kv_heads;
   a->d = c->head_dim;
   a->page_size = c->page_size;
+  a->use_k = c->signal != EPIKV_SIGNAL_KV_VAL;
+  a->use_v = c->signal == EPIKV_SIGNAL_LAGKV || c->signal == EPIKV_SIGNAL_KV_VAL;
+  a->lag = uses_range(c->signal);
   a->eps = c->eps;
   a->n_tok_in = (const int32_t*)state_in;
   a->range_in = (const float*)((const char*)state_in + L.off[3]);

@@ -50,9 +50,10 @@ struct ScoreLagArgs {
   int64_t ld_pt;
   const int32_t* n_cached;
   int32_t B, C, L, H, d, page_size;
+  int32_t use_k, use_v, lag;               // tensors used; lag normalisation
   float eps;
   const int32_t* n_tok_in;
-  const float* range_in;                   // [2][B][L][2][H][d]
+  const float* range_in;                   // [2][B][L][2][H][d] (lag only)
   float* range_out;
   float* partial;                          // [B][2L][C]
 };

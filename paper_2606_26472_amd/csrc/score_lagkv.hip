@@ -1,14 +1,18 @@
-// Lag-normalised key+value variance, Sec. 3.3 (Lag-KV):
-//   x~ = (x - mn) / (mx - mn + eps)   per channel, with (mn, mx) the range
-//        of the previous chunk at the same (layer, K|V, head, channel);
+// KV-vector signals, Sec. 3.3 and Table 1:
+//   Lag-KV      x~ = (x - mn) / (mx - mn + eps) per channel, with (mn, mx) the
+//               range of the previous chunk at the same (layer, K|V, head,
+//               channel), for keys and values;
+//   lag-kv-key  the same, keys only;
+//   KV-key/val  x~ = x, keys (values) only;
 //   v(t, l, kv, h) = population variance of x~ over the head dimension;
-//   q(t) = mean over (layer, head) of v(t, l, K, h) + v(t, l, V, h).
-// The chunk's own per-channel range is written out as the next chunk's
-// reference.  The first chunk of a stream, with no previous chunk, is
-// normalised by its own range.
+//   q(t) = mean over (layer, head) of the sum of v over the used tensors.
+// For the lag-normalised signals the chunk's own per-channel range is written
+// out as the next chunk's reference; the first chunk of a stream, with no
+// previous chunk, is normalised by its own range.
 //
 // Kernel 1: one 256-thread workgroup per (layer, K|V) plane and sequence
-// streams the chunk's rows of that plane from the paged pool.  Thread i owns
+// streams the chunk's rows of that plane from the paged pool (planes of an
+// unused tensor only zero their partial sums).  Thread i owns
 // 8 channels (one 16-byte column) of a row; the d/8 lanes of one head reduce
 // the variance with butterfly shuffles (two passes: mean, then squared
 // deviations), and per-(token, head) variances go to LDS.  The workgroup
@@ -50,6 +54,11 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
 
   float* vbuf = lds;                           // [C][H]
   float* cmb = lds + a.C * a.H;                // [2][rpp][HD] range combine
+  float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
+  if ((kv == 0 && !a.use_k) || (kv == 1 && !a.use_v)) {
+    for (int r = tid; r < a.C; r += kScoreThreads) part[r] = 0.f;
+    return;
+  }
 
   const int N = a.n_cached[b];
   const int start = N - a.C;
@@ -58,7 +67,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int32_t* pt = a.pt + (int64_t)b * a.ld_pt;
   const int64_t half = (int64_t)a.B * a.L * 2 * HD;
   const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
-  const bool fresh = a.n_tok_in[b] <= 0;
+  const bool fresh = a.lag && a.n_tok_in[b] <= 0;
 
   // Address of this thread's column of chunk row r, or nullptr.
   auto row_ptr = [&](int r) -> const char* {
@@ -117,11 +126,17 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
       mn[e] = cmn[e];
       mx[e] = cmx[e];
     }
-  } else {
+  } else if (a.lag) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       mn[e] = a.range_in[rbase + e];
       mx[e] = a.range_in[half + rbase + e];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = 0.f;
+      mx[e] = 0.f;
     }
   }
   float den[8];
@@ -143,7 +158,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
       for (int e = 0; e < 8; ++e) {
         cmn[e] = fminf(cmn[e], x[e]);
         cmx[e] = fmaxf(cmx[e], x[e]);
-        x[e] = (x[e] - mn[e]) / den[e];
+        if (a.lag) x[e] = (x[e] - mn[e]) / den[e];
       }
     } else {
 #pragma unroll
@@ -163,16 +178,16 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
     if (live && (col % gl) == 0) vbuf[r * a.H + head] = p ? var : 0.f;
   }
   __syncthreads();
-  combine();
-
-  if (ro == 0) {
+  if (a.lag) {
+    combine();
+    if (ro == 0) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      a.range_out[rbase + e] = cmn[e];
-      a.range_out[half + rbase + e] = cmx[e];
+      for (int e = 0; e < 8; ++e) {
+        a.range_out[rbase + e] = cmn[e];
+        a.range_out[half + rbase + e] = cmx[e];
+      }
     }
   }
-  float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
   for (int r = tid; r < a.C; r += kScoreThreads) {
     float s = 0.f;
     for (int h = 0; h < a.H; ++h) s += vbuf[r * a.H + h];

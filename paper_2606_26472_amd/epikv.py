@@ -29,6 +29,9 @@ SEQ_RANGE = 2
 
 SIGNAL_HS = 0
 SIGNAL_LAGKV = 1
+SIGNAL_KV_KEY = 2
+SIGNAL_KV_VAL = 3
+SIGNAL_LAGKV_KEY = 4
 SMOOTH_Z = 0
 SMOOTH_MEAN = 1
 SMOOTH_RAW = 2
@@ -296,7 +299,7 @@ def state_sections(cfg: Cfg, state):
     """Typed views of a uint8 state tensor (CPU or device):
     dict(n_tok [B] int32, ring [B][n_sig][w-1] float32,
          h_prev [B][n_band][D] int16 (HS), range [2][B][L][2][H][d] float32
-         (Lag-KV))."""
+         (lag-normalised KV signals))."""
     import torch
     off = state_layout(cfg)
     B, w = cfg.batch, cfg.window
@@ -310,7 +313,7 @@ def state_sections(cfg: Cfg, state):
         nh = B * nb * cfg.hidden
         out["h_prev"] = state[off[2]:off[2] + 2 * nh].view(torch.int16).view(
             B, nb, cfg.hidden)
-    else:
+    elif cfg.signal in (SIGNAL_LAGKV, SIGNAL_LAGKV_KEY):
         shp = (2, B, cfg.n_layers, 2, cfg.n_kv_heads, cfg.head_dim)
         n = 1
         for s in shp:

@@ -294,9 +294,18 @@ def test_compact_matches_oracle_bytes(E, page):
 # ---------------------------------------------------------------------------
 # score (Lag-KV): Sec. 3.3
 # ---------------------------------------------------------------------------
-def test_lagkv_matches_oracle(E):
+KV_SIGNALS = {  # name: (use keys, use values, lag-normalised)
+    "lagkv": (True, True, True), "kv_key": (True, False, False),
+    "kv_val": (False, True, False), "lagkv_key": (True, False, True)}
+
+
+@pytest.mark.parametrize("signal", list(KV_SIGNALS))
+def test_kv_signals_match_oracle(E, signal):
     import torch
-    print("lagkv", flush=True)
+    print(f"kv signal {signal}", flush=True)
+    use_k, use_v, lag = KV_SIGNALS[signal]
+    sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
+              "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
     g = synth.rng(500)
     L, H, d, page, B, C, w = 4, 8, 128, 16, 2, 64, 64
     n_chunks = 3
@@ -317,7 +326,7 @@ def test_lagkv_matches_oracle(E):
         tok.append(rows)
         pos = np.arange(Ns[b])
         pool[:, :, pt[b, pos // page], pos % page] = rows.transpose(1, 2, 0, 3)
-    cfg = E.default_cfg(batch=B, n_layers=L, signal=E.SIGNAL_LAGKV,
+    cfg = E.default_cfg(batch=B, n_layers=L, signal=sig_id,
                         smoothing=E.SMOOTH_MEAN, budget=4096)
     st = [torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
           for _ in range(2)]
@@ -341,19 +350,30 @@ def test_lagkv_matches_oracle(E):
         _sync()
         got_q = host(sig)[0]
         got_s = host(scores)
-        rng_out = E.state_sections(cfg, st[1].cpu())["range"].numpy()
+        secs = E.state_sections(cfg, st[1].cpu())
         for b in range(B):
             lo = n_cached[b] - C
             rows = O.bf16_to_float64(tok[b][lo:lo + C])   # [C][L][2][HD]
             k = rows[:, :, 0].reshape(C, L, H, d)
             v = rows[:, :, 1].reshape(C, L, H, d)
-            s_ref, q_ref, own = O.lagkv_chunk_scores(
-                k, v, prev_range[b], prior[b], O.SMOOTH_MEAN, w, cfg.eps)
+            s_ref, q_ref, own = O.kv_chunk_scores(
+                k, v, use_k, use_v, lag, prev_range[b], prior[b],
+                O.SMOOTH_MEAN, w, cfg.eps)
             assert _close(got_q[b], q_ref) <= TOL, (j, b)
             assert _close(got_s[b, lo:lo + C], s_ref) <= TOL, (j, b)
-            mn, mx = own
-            assert np.array_equal(rng_out[0, b], mn.astype(np.float32))
-            assert np.array_equal(rng_out[1, b], mx.astype(np.float32))
+            if lag:
+                mn, mx = own
+                rng_out = secs["range"].numpy()
+                if use_k:
+                    assert np.array_equal(rng_out[0, b][:, 0],
+                                          mn[:, 0].astype(np.float32))
+                    assert np.array_equal(rng_out[1, b][:, 0],
+                                          mx[:, 0].astype(np.float32))
+                if use_v:
+                    assert np.array_equal(rng_out[0, b][:, 1],
+                                          mn[:, 1].astype(np.float32))
+                    assert np.array_equal(rng_out[1, b][:, 1],
+                                          mx[:, 1].astype(np.float32))
             prev_range[b] = own
             prior[b] = np.concatenate([prior[b], q_ref])[-(w - 1):]
         st = [st[1], st[0]]

@@ -343,6 +343,47 @@ def test_lagkv_first_chunk_uses_own_range():
     assert s[0] == q[0]
 
 
+def test_kv_variance_closed_forms():
+    # Channels alternating +a / -a have population variance a^2 in every
+    # head, whatever the layer: KV-key gives a_k^2, KV-val a_v^2, both
+    # together their sum; the lag-normalised key-only signal of a token at
+    # the previous chunk's extremes gives 1/4 (times the eps factor).
+    L, H, d = 3, 2, 8
+    sign = np.where(np.arange(d) % 2 == 0, 1.0, -1.0)
+    k = np.broadcast_to(2.0 * sign, (1, L, H, d)).copy()
+    v = np.broadcast_to(0.5 * sign, (1, L, H, d)).copy()
+    assert O.kv_variance_signal(k, v, True, False)[0] == 4.0
+    assert O.kv_variance_signal(k, v, False, True)[0] == 0.25
+    assert O.kv_variance_signal(k, v, True, True)[0] == 4.25
+    mn = np.full((L, 2, H, d), -2.0)
+    mx = np.full((L, 2, H, d), 2.0)
+    r = 4.0 / (4.0 + EPS)
+    q = O.kv_variance_signal(k, v, True, False, (mn, mx))[0]
+    assert q == pytest.approx(0.25 * r * r, rel=1e-14)
+    # the lag-normalised key + value signal is the Lag-KV signal
+    g = synth.rng(19)
+    k2, v2 = _lag_shapes(g)
+    rng2 = O.chunk_range(*_lag_shapes(g))
+    assert np.allclose(O.kv_variance_signal(k2, v2, True, True, rng2),
+                       O.lagkv_signal(k2, v2, *rng2), rtol=1e-14)
+
+
+def test_kv_variance_raw_is_not_scale_invariant_but_lag_is():
+    # KV-key tracks magnitude (scaling the keys by c scales q by c^2); the
+    # lag-normalised variant removes it (Sec. 3.3).
+    g = synth.rng(20)
+    prev_k, prev_v = _lag_shapes(g)
+    k, v = _lag_shapes(g)
+    q1 = O.kv_variance_signal(k, v, True, False)
+    q3 = O.kv_variance_signal(3 * k, v, True, False)
+    assert np.allclose(q3, 9 * q1, rtol=1e-12)
+    r1 = O.chunk_range(prev_k, prev_v)
+    r3 = O.chunk_range(3 * prev_k, prev_v)
+    assert np.allclose(O.kv_variance_signal(3 * k, v, True, False, r3, 0.0),
+                       O.kv_variance_signal(k, v, True, False, r1, 0.0),
+                       rtol=1e-12)
+
+
 # ---------------------------------------------------------------------------
 # Which positions survive (Sec. 3.1, Sec. 3.3, App. D)
 # ---------------------------------------------------------------------------
