@@ -1,0 +1,114 @@
+"""epikv_evict_step under HIP graph capture.
+
+The step enqueues only kernels (no memset, no allocation, no host
+synchronisation), so a caller can capture it once and replay it.  Every
+replay -- with unrelated eager work and synchronisations between replays --
+must reproduce the eager step bit for bit.
+"""
+import numpy as np
+import pytest
+
+import synth
+from harness import dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def E():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26472_amd import epikv
+    epikv.lib()
+    return epikv
+
+
+@pytest.mark.parametrize("signal", ["hs", "lagkv"])
+def test_graph_replays_match_eager(E, signal):
+    import torch
+    print(f"graph capture {signal}", flush=True)
+    g = synth.rng(800)
+    B, C, K, page, L, H, d, D = 3, 64, 256, 16, 4, 8, 128, 512
+    na, nb = 2, 2
+    lengths = np.array([700, 300, 200])
+    ld_s = int(lengths.max())
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    pool = synth.random_bits16(g, (L, 2, n_src, page, H * d))
+    sc = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    if signal == "hs":
+        cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_band_a=na,
+                            n_band_b=nb, budget=K)
+        hid = dev(synth.f32_to_bf16_bits(
+            g.standard_normal((na + nb, B, C, D)).astype(np.float32)))
+        hidden = [hid[l] for l in range(na + nb)]
+    else:
+        cfg = E.default_cfg(batch=B, n_layers=L, signal=E.SIGNAL_LAGKV,
+                            smoothing=E.SMOOTH_MEAN, budget=K)
+        hidden = None
+    st_in = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
+    E.epikv_state_init(cfg, st_in)
+    torch.cuda.synchronize()
+    sec = E.state_sections(cfg, st_in)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32)).cuda()
+    sec["ring"][:] = torch.from_numpy(
+        (5.0 + g.standard_normal(tuple(sec["ring"].shape))).astype(
+            np.float32)).cuda()
+    st_out = torch.zeros_like(st_in)
+    src = dev(pool)
+    dst = torch.zeros((L, 2, n_dst, page, H * d), dtype=torch.int16,
+                      device="cuda")
+    scores = dev(sc)
+    dsc = torch.zeros_like(scores)
+    keep = torch.zeros((B, K), dtype=torch.int32, device="cuda")
+    n_keep = torch.zeros(B, dtype=torch.int32, device="cuda")
+    status = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    io = E.make_step_io(
+        C, hidden, D, C * D, dev(lengths.astype(np.int32)),
+        torch.zeros(B, dtype=torch.int32, device="cuda"),
+        E.pool_of(src.view(L, 2, n_src, page, H, d)), dev(src_pt),
+        src_pt.shape[1], E.pool_of(dst.view(L, 2, n_dst, page, H, d)),
+        dev(dst_pt), dst_pt.shape[1], scores, ld_s, st_in, st_out, keep,
+        n_keep, status, ws, ws_n, dst_scores=dsc)
+    outs = (scores, dsc, keep, n_keep, status, st_out, dst)
+
+    def snapshot():
+        torch.cuda.synchronize()
+        return [host(t).copy() for t in outs]
+
+    def clobber():
+        for t in outs:
+            t.view(torch.uint8).fill_(0x5B)
+
+    # every run starts from the same bytes in the outputs (the step leaves
+    # slots past n_keep and the state's padding untouched)
+    clobber()
+    scores.copy_(dev(sc))
+    E.epikv_evict_step(cfg, io)
+    eager = snapshot()
+    # capture on a side stream (warm it up first, as graph capture requires)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        E.epikv_evict_step(cfg, io)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        E.epikv_evict_step(cfg, io)
+    junk = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        clobber()
+        # the scores of the older tokens are inputs: restore them
+        scores.copy_(dev(sc))
+        graph.replay()
+        got = snapshot()
+        for a, b in zip(got, eager):
+            assert a.tobytes() == b.tobytes(), rep    # bytewise: NaN-safe
+        junk = junk * 1.0001 + 1.0              # unrelated eager work
+        torch.cuda.synchronize()
