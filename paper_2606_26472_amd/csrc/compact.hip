@@ -15,7 +15,10 @@
 //            then streams the row's 16-byte columns of every plane: a single
 //            dependent load before the data, so short-lived workgroups keep
 //            HBM busy.  Loads and stores are non-temporal: each byte is
-//            touched once.
+//            touched once.  The hardware deals workgroups to the 8 XCDs
+//            round-robin; the gather remaps its block index so that each XCD
+//            streams one contiguous range of destination slots (measured
+//            2-4% faster than the interleaved order).
 #include "epikv_internal.h"
 
 namespace epikv {
@@ -70,7 +73,12 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int b = blockIdx.z;
-  const int j = blockIdx.x * kCompactWaves + wave;
+  // XCD-aware: hardware places block x on XCD x % 8; give each XCD a
+  // contiguous range of slot groups.
+  const int nx = gridDim.x;
+  int bx = blockIdx.x;
+  if ((nx & 7) == 0) bx = (bx & 7) * (nx >> 3) + (bx >> 3);
+  const int j = bx * kCompactWaves + wave;
   const int row_vec = a.row_bytes >> 4;
   // The record of slot min(j, K-1) is always readable, so it is fetched
   // together with n_keep instead of after it.
