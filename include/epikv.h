@@ -75,7 +75,10 @@ typedef enum epikv_signal {
 typedef enum epikv_smoothing {
   EPIKV_SMOOTH_Z = 0,       /* rolling z-score, Eq. 3 (EpiKV) */
   EPIKV_SMOOTH_MEAN = 1,    /* rolling mean, Eq. 2 (HS-variance, KV family) */
-  EPIKV_SMOOTH_RAW = 2      /* no smoothing (App. E "raw") */
+  EPIKV_SMOOTH_RAW = 2,     /* no smoothing (App. E "raw") */
+  EPIKV_SMOOTH_EMA = 3      /* exponential moving average (App. E, alpha 0.9):
+                               y = alpha*y_prev + (1-alpha)*x, y = x at the
+                               stream's first sample */
 } epikv_smoothing;
 
 #define EPIKV_MAX_BAND 32   /* band layers per call */
@@ -106,6 +109,7 @@ typedef struct epikv_cfg {
   int32_t smoothing;    /* epikv_smoothing */
   int32_t budget;       /* K >= 1: positions kept per sequence */
   int32_t recent;       /* R >= 0, or -1 for min(128, K/4) (App. D) */
+  float ema_alpha;      /* EMA weight of the previous average, [0, 1] (paper: 0.9) */
 } epikv_cfg;
 
 /*
@@ -126,7 +130,7 @@ typedef struct epikv_pool {
 
 /* Fill *cfg with the paper's setting: 32 layers, D = 4096, 8 KV heads x 128,
  * 16-token pages, Band A = 7 layers, Band B = 8 layers, w = 64, eps = 1e-6,
- * HS signal, z-score smoothing, R = min(128, K/4).  batch and budget are set
+ * HS signal, z-score smoothing, R = min(128, K/4), EMA alpha = 0.9.  batch and budget are set
  * to 1 and 4096.  Returns EPIKV_EINVAL_NULL if cfg is NULL. */
 int epikv_default_cfg(epikv_cfg* cfg);
 
@@ -148,6 +152,9 @@ int epikv_check_cfg(const epikv_cfg* cfg);
  *   [3] float range[2][B][L][2][H][d] lag-normalised signals: per-channel
  *                                 min (first half) and max of the previous
  *                                 chunk
+ *   [4] float ema[B][n_sig]       the running average after the last sample
+ *                                 (EMA smoothing; carried unchanged in the
+ *                                 other modes)
  * n_sig = n_band_a + n_band_b for HS, 1 for the KV-vector signals.  An HS
  * stream yields a sample for every token but its first (which has no
  * predecessor); a KV-vector stream for every token.  Sections a signal does
@@ -156,9 +163,9 @@ int epikv_check_cfg(const epikv_cfg* cfg);
  */
 size_t epikv_state_bytes(const epikv_cfg* cfg);
 
-/* Byte offsets of the four state sections (host array of 4), see above.
+/* Byte offsets of the five state sections (host array of 5), see above.
  * Returns EPIKV_OK or a host error code. */
-int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]);
+int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
 
 /* Device scratch that epikv_evict_step (and epikv_score) needs for a chunk
  * of `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
@@ -219,7 +226,8 @@ int epikv_score(const epikv_cfg* cfg, int32_t chunk,
  * For each signal row the new samples follow the w-1 carried in
  * state_in.ring; each token's window is the last min(w, available) samples
  * up to and including its own.  Z: (x - mu) / (sigma + eps) with the
- * population sigma; MEAN: mu; RAW: x.  Tokens without a sample get 0.  The
+ * population sigma; MEAN: mu; RAW: x; EMA: the running average carried in
+ * state_in.ema.  Tokens without a sample get 0.  The
  * frozen score s = mean over Band A rows - mean over Band B rows (KV-vector
  * signals: the single row) is written to scores[b*ld_s + n_cached[b] - chunk + c].
  * Sequences with n_cached < chunk or n_cached > ld_s are skipped.

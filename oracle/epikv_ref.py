@@ -47,6 +47,9 @@ READINGS = {
            "NaN ranks below every number, NaNs tie and break by position.",
     "R13": "The rebuilt cache is order preserving (App. H) and written out of "
            "place.",
+    "R17": "EMA smoothing (App. E, alpha = 0.9): y(t) = alpha * y(t-1) + "
+           "(1 - alpha) * x(t), starting at the stream's first sample "
+           "(y = x); tokens without a sample leave y unchanged and get 0.",
     "R14": "Lag-KV: each channel of a token's key and value is min-max "
            "normalised with the previous chunk's per-(layer, K|V, head, "
            "channel) range plus eps; the population variance over the head "
@@ -143,6 +146,21 @@ def rolling_zscore(x, w=WINDOW_DEFAULT, eps=EPS_DEFAULT):
 SMOOTH_Z = "z"        # Eq. 3 (EpiKV)
 SMOOTH_MEAN = "mean"  # Eq. 2 (HS-variance, KV family)
 SMOOTH_RAW = "raw"    # unsmoothed signal (App. E, "raw")
+SMOOTH_EMA = "ema"    # exponential moving average (App. E, alpha = 0.9)
+EMA_ALPHA = 0.9
+
+
+def ema(x, alpha=EMA_ALPHA, y_before=None):
+    """Exponential moving average of a sample sequence (App. E, R17):
+    y(t) = alpha * y(t-1) + (1 - alpha) * x(t).  y_before is the average
+    just before x[0] (None: the sequence starts the stream, y(0) = x(0))."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.empty(x.size, dtype=np.float64)
+    y = y_before
+    for i in range(x.size):
+        y = x[i] if y is None else alpha * y + (1.0 - alpha) * x[i]
+        out[i] = y
+    return out
 
 
 def smooth(samples, mode, w=WINDOW_DEFAULT, eps=EPS_DEFAULT):
@@ -153,23 +171,32 @@ def smooth(samples, mode, w=WINDOW_DEFAULT, eps=EPS_DEFAULT):
         return rolling_mean(samples, w)
     if mode == SMOOTH_RAW:
         return np.asarray(samples, dtype=np.float64).copy()
+    if mode == SMOOTH_EMA:
+        return ema(samples)
     raise ValueError(f"unknown smoothing mode {mode!r}")
 
 
 def smooth_stream(prior, new, has_sample, mode, w=WINDOW_DEFAULT,
-                  eps=EPS_DEFAULT):
+                  eps=EPS_DEFAULT, ema_before=None):
     """Smoothed value of each new token of one signal row.
 
     prior      : earlier samples of the stream, chronological (only the last
                  w-1 can enter a window of a new token).
     new        : per-token signal of the new tokens.
     has_sample : which new tokens carry a sample (R7); the others get 0.
+    ema_before : EMA mode only: the running average after the prior samples
+                 (default: computed from `prior`).
     """
     new = np.asarray(new, dtype=np.float64)
     has_sample = np.asarray(has_sample, dtype=bool)
     prior = np.asarray(prior, dtype=np.float64)
-    seq = np.concatenate([prior, new[has_sample]])
-    sm = smooth(seq, mode, w, eps)[prior.size:]
+    if mode == SMOOTH_EMA:
+        if ema_before is None and prior.size:
+            ema_before = ema(prior)[-1]
+        sm = ema(new[has_sample], y_before=ema_before)
+    else:
+        seq = np.concatenate([prior, new[has_sample]])
+        sm = smooth(seq, mode, w, eps)[prior.size:]
     out = np.zeros(new.size, dtype=np.float64)
     out[has_sample] = sm
     return out

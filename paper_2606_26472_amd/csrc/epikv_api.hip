@@ -38,9 +38,11 @@ int row_bytes(const epikv_cfg* c) { return c->n_kv_heads * c->head_dim * 2; }
 
 int pages_for(int64_t tokens, int page_size) { return (int)((tokens + page_size - 1) / page_size); }
 
+constexpr int kSections = 5;
+
 struct Layout {
-  size_t off[4];
-  size_t size[4];
+  size_t off[kSections];
+  size_t size[kSections];
   size_t total;
 };
 
@@ -53,8 +55,9 @@ Layout state_layout(const epikv_cfg* c) {
   L.size[3] = uses_range(c->signal)
                   ? 4 * 2 * B * (size_t)c->n_layers * 2 * (size_t)c->n_kv_heads * (size_t)c->head_dim
                   : 0;
+  L.size[4] = 4 * B * (size_t)n_sig(c);
   size_t o = 0;
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kSections; ++i) {
     L.off[i] = o;
     o = align_up(o + L.size[i]);
   }
@@ -78,7 +81,8 @@ size_t partial_bytes(const epikv_cfg* c, int chunk) {
 int check_cfg(const epikv_cfg* c) {
   if (!c) return EPIKV_EINVAL_NULL;
   if (c->signal < EPIKV_SIGNAL_HS || c->signal > EPIKV_SIGNAL_LAGKV_KEY) return EPIKV_EINVAL_PARAM;
-  if (c->smoothing < EPIKV_SMOOTH_Z || c->smoothing > EPIKV_SMOOTH_RAW) return EPIKV_EINVAL_PARAM;
+  if (c->smoothing < EPIKV_SMOOTH_Z || c->smoothing > EPIKV_SMOOTH_EMA) return EPIKV_EINVAL_PARAM;
+  if (!(c->ema_alpha >= 0.f && c->ema_alpha <= 1.f)) return EPIKV_EINVAL_PARAM;
   if (c->window < 1 || c->window > EPIKV_MAX_WINDOW) return EPIKV_EINVAL_PARAM;
   if (!(c->eps >= 0.f) || !isfinite(c->eps)) return EPIKV_EINVAL_PARAM;
   if (c->budget < 1) return EPIKV_EINVAL_PARAM;
@@ -253,6 +257,9 @@ ZscoreArgs zscore_args(const epikv_cfg* c, int32_t chunk, const float* sig, cons
   a.ring_in = (const float*)((const char*)state_in + L.off[1]);
   a.n_tok_out = (int32_t*)state_out;
   a.ring_out = (float*)((char*)state_out + L.off[1]);
+  a.ema_in = (const float*)((const char*)state_in + L.off[4]);
+  a.ema_out = (float*)((char*)state_out + L.off[4]);
+  a.alpha = c->ema_alpha;
   a.scores = scores;
   a.ld_s = ld_s;
   a.smoothed = smoothed;
@@ -392,6 +399,7 @@ EPIKV_EXPORT int epikv_default_cfg(epikv_cfg* cfg) {
   cfg->smoothing = EPIKV_SMOOTH_Z;
   cfg->budget = 4096;
   cfg->recent = -1;
+  cfg->ema_alpha = 0.9f;
   return EPIKV_OK;
 }
 
@@ -416,12 +424,12 @@ EPIKV_EXPORT size_t epikv_state_bytes(const epikv_cfg* cfg) {
   return state_layout(cfg).total;
 }
 
-EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[4]) {
+EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]) {
   const int st = check_cfg(cfg);
   if (st) return st;
   if (!offsets) return EPIKV_EINVAL_NULL;
   const Layout L = state_layout(cfg);
-  for (int i = 0; i < 4; ++i) offsets[i] = L.off[i];
+  for (int i = 0; i < kSections; ++i) offsets[i] = L.off[i];
   return EPIKV_OK;
 }
 

@@ -74,6 +74,9 @@ struct ZscoreArgs {
   const float* ring_in;                    // [B][n_sig][w-1]
   int32_t* n_tok_out;
   float* ring_out;
+  const float* ema_in;                     // [B][n_sig] running averages
+  float* ema_out;
+  float alpha;                             // EMA weight of the previous average
   float* scores;
   int64_t ld_s;
   float* smoothed;                         // optional [n_sig][B][C]

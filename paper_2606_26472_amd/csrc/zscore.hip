@@ -21,6 +21,7 @@ namespace epikv {
 namespace {
 
 constexpr int kWaves = kZscoreThreads / 64;
+constexpr int kZscoreWaves = kWaves;
 constexpr int kSlice = EPIKV_MAX_WINDOW - 1 + kZscoreTile;
 
 __global__ __launch_bounds__(kZscoreThreads) void k_zscore(ZscoreArgs a) {
@@ -118,11 +119,98 @@ __global__ __launch_bounds__(kZscoreThreads) void k_zscore(ZscoreArgs a) {
     if (N >= a.C && (int64_t)N <= a.ld_s) a.scores[(int64_t)b * a.ld_s + (N - a.C) + c] = s;
   }
   if (last_tile && tid == 0) a.n_tok_out[b] = n_tok + a.C;
+  if (last_tile && tid < a.n_sig)
+    a.ema_out[(int64_t)b * a.n_sig + tid] = a.ema_in[(int64_t)b * a.n_sig + tid];
+}
+
+// EMA smoothing (App. E): y(t) = alpha*y(t-1) + (1-alpha)*x(t), y = x at the
+// stream's first sample.  One 1024-thread workgroup per sequence walks the
+// chunk in 64-token tiles; for each signal row a wavefront turns its tile
+// into per-token affine maps y -> A*y + Bc (a token without a sample is the
+// identity) and composes them with a lane-wise inclusive scan, so the tile's
+// averages follow exactly from the average carried in from the previous
+// tile.  The per-row values meet in LDS for the band combination.
+__global__ __launch_bounds__(kZscoreThreads) void k_ema(ZscoreArgs a) {
+  __shared__ float carry[EPIKV_MAX_BAND];
+  __shared__ float vals[EPIKV_MAX_BAND][kZscoreTile];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int b = blockIdx.y;
+  const int wm1 = a.w - 1;
+  const int n_tok = max(a.n_tok_in[b], 0);
+  const int c0 = (a.hs && n_tok == 0) ? 1 : 0;
+  const int64_t prior = a.hs ? (int64_t)max(n_tok - 1, 0) : (int64_t)n_tok;
+  const float al = a.alpha, bl = 1.0f - a.alpha;
+  if (tid < a.n_sig) carry[tid] = a.ema_in[(int64_t)b * a.n_sig + tid];
+  const int N = a.n_cached[b];
+  const bool write_scores = N >= a.C && (int64_t)N <= a.ld_s;
+  const int rounds = (a.n_sig + kZscoreWaves - 1) / kZscoreWaves;
+  const int tiles = (a.C + kZscoreTile - 1) / kZscoreTile;
+  __syncthreads();
+  for (int tile = 0; tile < tiles; ++tile) {
+    const int c = tile * kZscoreTile + lane;
+    const bool has = c < a.C && c >= c0;
+    // the stream's first sample starts the average
+    const bool first = prior == 0 && c == c0;
+    for (int rd = 0; rd < rounds; ++rd) {
+      const int l = rd * kZscoreWaves + wave;
+      if (l < a.n_sig) {
+        const float x = has ? a.sig[((int64_t)l * a.B + b) * a.C + c] : 0.f;
+        float A = has ? (first ? 0.f : al) : 1.f;
+        float Bc = has ? (first ? x : bl * x) : 0.f;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const float pa = __shfl_up(A, off, 64);
+          const float pb = __shfl_up(Bc, off, 64);
+          if (lane >= off) {
+            Bc = fmaf(A, pb, Bc);
+            A = A * pa;
+          }
+        }
+        const float y = fmaf(A, carry[l], Bc);
+        const float v = has ? y : 0.f;
+        vals[l][lane] = v;
+        if (a.smoothed && c < a.C) a.smoothed[((int64_t)l * a.B + b) * a.C + c] = v;
+        const float y_last = __shfl(y, 63, 64);
+        if (lane == 0) carry[l] = y_last;
+      }
+    }
+    __syncthreads();
+    if (tid < kZscoreTile && c < a.C && write_scores) {
+      float sa = 0.f, sb = 0.f;
+      for (int l = 0; l < a.n_a; ++l) sa += vals[l][tid];
+      for (int l = a.n_a; l < a.n_sig; ++l) sb += vals[l][tid];
+      float s = sa / (float)a.n_a;
+      if (a.n_b > 0) s -= sb / (float)a.n_b;
+      a.scores[(int64_t)b * a.ld_s + (N - a.C) + c] = s;
+    }
+    __syncthreads();
+  }
+  // carried state: averages, sample ring, token count
+  if (tid < a.n_sig) a.ema_out[(int64_t)b * a.n_sig + tid] = carry[tid];
+  const int64_t total_out = prior + (a.C - c0);
+  const int cnt_out = (int)min((int64_t)wm1, total_out);
+  for (int i = tid; i < a.n_sig * wm1; i += kZscoreThreads) {
+    const int l = i / wm1;
+    const int k = i - l * wm1;
+    const int j = a.C + k;  // index in [ring | chunk signal]
+    float v = 0.f;
+    if ((wm1 - 1 - k) < cnt_out)
+      v = j < wm1 ? a.ring_in[((int64_t)b * a.n_sig + l) * wm1 + j]
+                  : a.sig[((int64_t)l * a.B + b) * a.C + (j - wm1)];
+    a.ring_out[((int64_t)b * a.n_sig + l) * wm1 + k] = v;
+  }
+  if (tid == 0) a.n_tok_out[b] = n_tok + a.C;
 }
 
 }  // namespace
 
 hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s) {
+  if (a.mode == EPIKV_SMOOTH_EMA) {
+    hipLaunchKernelGGL(k_ema, dim3(1, a.B), dim3(kZscoreThreads), 0, s, a);
+    return hipGetLastError();
+  }
   dim3 grid((a.C + kZscoreTile - 1) / kZscoreTile, a.B);
   hipLaunchKernelGGL(k_zscore, grid, dim3(kZscoreThreads), 0, s, a);
   return hipGetLastError();

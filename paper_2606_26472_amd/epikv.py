@@ -35,6 +35,7 @@ SIGNAL_LAGKV_KEY = 4
 SMOOTH_Z = 0
 SMOOTH_MEAN = 1
 SMOOTH_RAW = 2
+SMOOTH_EMA = 3
 MAX_BAND = 32
 
 EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
@@ -58,7 +59,8 @@ class Cfg(ctypes.Structure):
                 ("n_band_a", ctypes.c_int32), ("n_band_b", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("eps", ctypes.c_float),
                 ("signal", ctypes.c_int32), ("smoothing", ctypes.c_int32),
-                ("budget", ctypes.c_int32), ("recent", ctypes.c_int32)]
+                ("budget", ctypes.c_int32), ("recent", ctypes.c_int32),
+                ("ema_alpha", ctypes.c_float)]
 
 
 class Pool(ctypes.Structure):
@@ -175,7 +177,7 @@ def state_bytes(cfg: Cfg) -> int:
 
 
 def state_layout(cfg: Cfg):
-    off = (ctypes.c_size_t * 4)()
+    off = (ctypes.c_size_t * 5)()
     _check(lib().epikv_state_layout(ctypes.byref(cfg), off),
            "epikv_state_layout")
     return [int(x) for x in off]
@@ -297,7 +299,7 @@ def n_sig(cfg: Cfg) -> int:
 
 def state_sections(cfg: Cfg, state):
     """Typed views of a uint8 state tensor (CPU or device):
-    dict(n_tok [B] int32, ring [B][n_sig][w-1] float32,
+    dict(n_tok [B] int32, ring [B][n_sig][w-1] float32, ema [B][n_sig],
          h_prev [B][n_band][D] int16 (HS), range [2][B][L][2][H][d] float32
          (lag-normalised KV signals))."""
     import torch
@@ -320,4 +322,7 @@ def state_sections(cfg: Cfg, state):
             n *= s
         out["range"] = state[off[3]:off[3] + 4 * n].view(torch.float32).view(
             *shp)
+    ne = B * n_sig(cfg)
+    out["ema"] = state[off[4]:off[4] + 4 * ne].view(torch.float32).view(
+        B, n_sig(cfg))
     return out

@@ -54,6 +54,7 @@ def test_default_cfg_is_the_papers_setting(E):
     c = E.default_cfg()
     assert (c.n_layers, c.hidden, c.n_kv_heads, c.head_dim) == (32, 4096, 8, 128)
     assert (c.n_band_a, c.n_band_b, c.window) == (7, 8, 64)
+    assert abs(c.ema_alpha - 0.9) < 1e-7
     assert c.recent == -1 and c.page_size == 16
     assert abs(c.eps - 1e-6) < 1e-12
     assert E.check_cfg(c) == 0
@@ -65,7 +66,8 @@ def test_default_cfg_is_the_papers_setting(E):
     ("signal", 5, -3), ("smoothing", 9, -3), ("batch", 0, -2),
     ("hidden", 4100, -2), ("hidden", 0, -2), ("head_dim", 96, -2),
     ("n_kv_heads", 0, -2), ("n_band_a", 0, -2), ("n_band_b", 30, -2),
-    ("page_size", 0, -2), ("page_size", 2048, -2), ("n_layers", 0, -2)])
+    ("page_size", 0, -2), ("page_size", 2048, -2), ("n_layers", 0, -2),
+    ("ema_alpha", 1.5, -3), ("ema_alpha", -0.1, -3), ("smoothing", 4, -3)])
 def test_check_cfg_rejects(E, field, value, code):
     c = E.default_cfg()
     setattr(c, field, value)
@@ -82,13 +84,15 @@ def test_check_cfg_null(E):
 def test_state_layout_sizes(E):
     c = E.default_cfg(batch=32)
     off = E.state_layout(c)
+    assert len(off) == 5
     assert off[0] == 0 and all(o % 256 == 0 for o in off)
+    assert E.state_bytes(c) - off[4] >= 4 * 32 * 15
     assert off[2] - off[1] >= 4 * 32 * 15 * 63
-    assert E.state_bytes(c) - off[2] >= 2 * 32 * 15 * 4096
+    assert off[3] - off[2] >= 2 * 32 * 15 * 4096
     lag = E.default_cfg(batch=8, signal=E.SIGNAL_LAGKV)
     off = E.state_layout(lag)
     assert off[3] == off[2]                # no h_prev section
-    assert E.state_bytes(lag) - off[3] >= 4 * 2 * 8 * 32 * 2 * 8 * 128
+    assert off[4] - off[3] >= 4 * 2 * 8 * 32 * 2 * 8 * 128
     assert E.workspace_bytes(c, 128) >= 4 * 15 * 32 * 128
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
     assert E.workspace_bytes(c, 0) == 0

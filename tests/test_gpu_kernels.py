@@ -91,7 +91,7 @@ def test_score_hs_matches_oracle(E, D, C, fresh, pad):
 # ---------------------------------------------------------------------------
 # zscore: Eqs. 2-3 and the band combination
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("mode", ["z", "mean", "raw"])
+@pytest.mark.parametrize("mode", ["z", "mean", "raw", "ema"])
 @pytest.mark.parametrize("C", [1, 7, 600])
 def test_zscore_matches_oracle(E, mode, C):
     import torch
@@ -99,8 +99,10 @@ def test_zscore_matches_oracle(E, mode, C):
     g = synth.rng(200 + C)
     B, na, nb, w = 4, 3, 2, 64
     nsig = na + nb
-    smode = {"z": E.SMOOTH_Z, "mean": E.SMOOTH_MEAN, "raw": E.SMOOTH_RAW}[mode]
-    omode = {"z": O.SMOOTH_Z, "mean": O.SMOOTH_MEAN, "raw": O.SMOOTH_RAW}[mode]
+    smode = {"z": E.SMOOTH_Z, "mean": E.SMOOTH_MEAN, "raw": E.SMOOTH_RAW,
+             "ema": E.SMOOTH_EMA}[mode]
+    omode = {"z": O.SMOOTH_Z, "mean": O.SMOOTH_MEAN, "raw": O.SMOOTH_RAW,
+             "ema": O.SMOOTH_EMA}[mode]
     cfg = E.default_cfg(batch=B, n_band_a=na, n_band_b=nb, smoothing=smode)
     n_tok = np.array([0, 10, 1000, 64], dtype=np.int32)
     # signal at the level of a 4096-wide hidden-state change: mean ~90x the
@@ -116,10 +118,14 @@ def test_zscore_matches_oracle(E, mode, C):
         priors.append(pb)
     ld_s = 2000
     n_cached = np.array([C, C + 5, 1500, ld_s], dtype=np.int32)
+    # carried running averages (EMA): any value for streams with a sample
+    ema_in = (90.0 + g.standard_normal((B, nsig))).astype(np.float32)
+    ema_in[0] = 0.0                       # fresh stream: nothing carried
     st_in = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8)
     sec = E.state_sections(cfg, st_in)
     sec["n_tok"][:] = torch.from_numpy(n_tok)
     sec["ring"][:] = torch.from_numpy(ring)
+    sec["ema"][:] = torch.from_numpy(ema_in)
     st_in = st_in.cuda()
     st_out = torch.zeros_like(st_in)
     scores = torch.full((B, ld_s), 123.0, device="cuda")
@@ -136,8 +142,11 @@ def test_zscore_matches_oracle(E, mode, C):
         if n_tok[b] == 0:
             has[0] = False
         rows = []
+        prior_samples = max(int(n_tok[b]) - 1, 0)
         for l in range(nsig):
-            r = O.smooth_stream(priors[b][l], sig[l, b], has, omode, w, 1e-6)
+            eb = float(ema_in[b, l]) if prior_samples > 0 else None
+            r = O.smooth_stream(priors[b][l], sig[l, b], has, omode, w, 1e-6,
+                                ema_before=eb)
             rows.append(r)
             worst = max(worst, _close(got_sm[l, b], r))
             # carried window: the last min(w-1, samples) samples
@@ -153,6 +162,18 @@ def test_zscore_matches_oracle(E, mode, C):
         # nothing outside the chunk's slots is written
         assert np.all(got_s[b, :N - C] == 123.0)
         assert np.all(got_s[b, N:] == 123.0)
+        if mode == "ema":
+            # the carried average after the chunk
+            seq_y = O.smooth_stream(priors[b][0], sig[0, b], has, omode,
+                                    ema_before=float(ema_in[b, 0])
+                                    if prior_samples > 0 else None)
+            last = seq_y[has][-1] if has.any() else (
+                ema_in[b, 0] if prior_samples > 0 else None)
+            if last is not None:
+                assert abs(float(out["ema"][b, 0]) - last) <= \
+                    TOL * max(1.0, abs(last))
+        else:
+            assert np.array_equal(out["ema"][b].numpy(), ema_in[b])
     assert worst <= TOL, worst
     assert np.array_equal(out["n_tok"].numpy(), n_tok + C)
 

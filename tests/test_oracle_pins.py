@@ -196,6 +196,26 @@ def test_rolling_mean_ramp_closed_form():
     assert m[0] == 2.0 and m[1] == 2.25
 
 
+def test_ema_closed_forms():
+    # step response: from y = 0, a unit step gives y(n) = 1 - alpha^(n+1)
+    a = O.EMA_ALPHA
+    y = O.ema(np.ones(50), a, y_before=0.0)
+    n = np.arange(50)
+    assert np.allclose(y, 1.0 - a ** (n + 1), rtol=1e-14, atol=0)
+    # a constant stream started fresh stays constant
+    assert np.all(O.ema(np.full(30, 2.5)) == 2.5)
+    # impulse response decays geometrically with ratio alpha
+    x = np.zeros(20)
+    x[0] = 1.0
+    y = O.ema(x, a, y_before=0.0)
+    assert np.allclose(y, (1 - a) * a ** np.arange(20), rtol=1e-14)
+    # carrying the average across chunks equals one pass
+    x = synth.rng(21).standard_normal(300)
+    full = O.ema(x)
+    part = O.ema(x[120:], y_before=O.ema(x[:120])[-1])
+    assert np.allclose(part, full[120:], rtol=1e-13)
+
+
 def test_smooth_stream_skips_tokens_without_sample():
     new = np.array([123.0, 1.0, 3.0])
     out = O.smooth_stream(np.zeros(0), new, np.array([False, True, True]),
