@@ -171,8 +171,9 @@ int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
  * of `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
 
-/* Device scratch of epikv_compact: 16 bytes per (sequence, kept slot),
- * B*K*16 rounded up to 256.  0 for an invalid cfg. */
+/* Device scratch of epikv_compact and epikv_compact_inplace: 16 bytes per
+ * (sequence, kept slot), B*K*16 rounded up to 256, then 8 bytes per sequence
+ * rounded up to 256.  0 for an invalid cfg. */
 size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg);
 
 /* Reset a state buffer of epikv_state_bytes(cfg) bytes to the start of a
@@ -285,6 +286,39 @@ int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src,
                   int64_t ld_s, int32_t* seq_status, void* workspace,
                   size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * epikv_compact_inplace -- the same rebuild inside the sequence's own pages
+ * (the move-minimising form of App. H's rebuild; no second pool).
+ *
+ * page_table (int32 [B][ld_pt]) maps the sequence's positions to pages of
+ * `pool` both before and after the call.  For every sequence with
+ * n_keep[b] > 0 and every j < min(n_keep[b], K): slot j receives, bit for
+ * bit, the row that position keep_idx[b][j] held before the call, for every
+ * layer, K and V.  keep_idx must be strictly ascending (as epikv_select
+ * writes it), so rows only move towards the front.  Slots before the first
+ * hole (the first j with keep_idx[b][j] != j) are not written, nor is any
+ * slot >= n_keep[b]: pages wholly inside that leading run -- for instance
+ * prefill pages shared between sequences and protected by n_prefix -- are
+ * never touched, and pages past ceil(n_keep / page_size) may be released by
+ * the caller afterwards.  scores (float [B][ld_s]) and pos (int32 [B][ld_s])
+ * are optional and move the same way, in place.
+ *
+ * Pages of one sequence must not be pages of another sequence unless they
+ * lie in that leading run.  A sequence whose keep_idx is not strictly
+ * ascending, reaches a page id outside [0, n_pages) or past ld_pt, or (with
+ * scores/pos) a position >= ld_s, is left untouched and flagged
+ * seq_status[b] = RANGE (when seq_status is given).  Sequences with
+ * n_keep[b] <= 0 are skipped.
+ * workspace: 16-byte aligned device scratch of at least
+ * epikv_compact_workspace_bytes(cfg) bytes, overlapping no other argument.
+ */
+int epikv_compact_inplace(const epikv_cfg* cfg, const epikv_pool* pool,
+                          const int32_t* page_table, int64_t ld_pt,
+                          const int32_t* keep_idx, const int32_t* n_keep,
+                          float* scores, int32_t* pos, int64_t ld_s,
+                          int32_t* seq_status, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+
 /* Arguments of one eviction step (host struct; pointers as above). */
 typedef struct epikv_step_io {
   int32_t chunk;                /* new tokens per sequence (eviction cadence) */
@@ -310,6 +344,11 @@ typedef struct epikv_step_io {
   int32_t* seq_status;          /* [B] */
   void* workspace;
   size_t workspace_bytes;       /* >= epikv_workspace_bytes(cfg, chunk) */
+  int32_t in_place;             /* nonzero: compact with epikv_compact_inplace
+                                   on src/src_pt; dst and dst_pt are ignored,
+                                   scores always follow their rows in place,
+                                   dst_scores must be NULL or scores, and
+                                   dst_pos must equal src_pos (moved in place) */
 } epikv_step_io;
 
 /*

@@ -47,6 +47,9 @@ READINGS = {
            "NaN ranks below every number, NaNs tie and break by position.",
     "R13": "The rebuilt cache is order preserving (App. H) and written out of "
            "place.",
+    "R18": "In-place rebuild (the move-minimising form): the retained rows "
+           "are packed to the front of the sequence's own pages in order; "
+           "slots past the retained count keep whatever they held.",
     "R17": "EMA smoothing (App. E, alpha = 0.9): y(t) = alpha * y(t-1) + "
            "(1 - alpha) * x(t), starting at the stream's first sample "
            "(y = x); tokens without a sample leave y unchanged and get 0.",
@@ -382,3 +385,23 @@ def compact_rows(rows, keep):
     R13).  `rows` may carry any trailing shape; copying is exact."""
     rows = np.asarray(rows)
     return rows[np.asarray(keep, dtype=np.int64)].copy()
+
+
+def first_hole(keep):
+    """First slot j whose retained position differs from j (len(keep) when
+    the retained set is a leading run).  Slots before it need no move."""
+    keep = np.asarray(keep, dtype=np.int64)
+    moved = np.nonzero(keep != np.arange(keep.size))[0]
+    return int(moved[0]) if moved.size else int(keep.size)
+
+
+def compact_rows_inplace(rows, keep):
+    """In-place order-preserving rebuild (App. H, R18): slot j < len(keep)
+    receives the row that position keep[j] held; every later slot keeps its
+    old row.  `rows` holds the sequence's rows before the rebuild (leading
+    axis = position); the result is a new array."""
+    rows = np.asarray(rows)
+    keep = np.asarray(keep, dtype=np.int64)
+    out = rows.copy()
+    out[:keep.size] = rows[keep]
+    return out

@@ -1,0 +1,210 @@
+// Order-preserving rebuild of the cache inside the sequence's own pages: the
+// move-minimising form of the App. H rebuild.  Slot j of sequence b receives
+// the row of position keep_idx[b][j]; keep_idx is strictly ascending, so
+// keep_idx[j] >= j and every row only moves towards the front.  Slots in
+// front of the first hole (keep_idx[j] == j) already hold their row and are
+// not touched, nor is anything at or past n_keep.
+//
+// Two kernels:
+//   check  one 1024-thread workgroup per sequence verifies that keep_idx is
+//          strictly ascending and that every page it reaches exists, writes
+//          the byte offsets of each moved row (source and destination, inside
+//          a plane) to the workspace together with the first hole, and moves
+//          the scores and positions.  A sequence that fails the check is left
+//          untouched and flagged RANGE.
+//   move   one wavefront per (sequence, plane, column slice) walks the moved
+//          slots in ascending order, a tile of T rows at a time: it loads the
+//          tile's source rows, waits until every load has returned, then
+//          stores them.  A store to slot j can only overwrite a row that a
+//          slot <= j reads; slots of this tile have read theirs, and slots of
+//          later tiles read rows past the end of this tile (their sources
+//          are >= their own slots).  So one wavefront per column slice moves
+//          its bytes without any barrier or second copy, and different
+//          slices, planes and sequences touch disjoint bytes.
+#include "epikv_internal.h"
+
+namespace epikv {
+namespace {
+
+// Every memory operation issued so far has completed: loaded values are in
+// registers and earlier stores are done.  The builtin (rather than inline
+// assembly) lets the compiler see that nothing is outstanding afterwards, so
+// it adds no waits of its own between the stores that follow; the empty asm
+// statements keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void wait_vmem() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
+  const int lo = __shfl((int)(uint32_t)(uint64_t)v, src);
+  const int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__global__ __launch_bounds__(kInplaceThreads) void k_inplace_check(InplaceArgs a) {
+  __shared__ int s_bad[kInplaceThreads / 64];
+  __shared__ int s_hole[kInplaceThreads / 64];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int b = blockIdx.x;
+  int32_t* info = a.info + 2 * b;
+  int nk = a.n_keep[b];
+  if (nk <= 0) {  // nothing kept, or a sequence select already refused
+    if (tid == 0) info[0] = info[1] = 0;
+    return;
+  }
+  nk = min(nk, a.K);
+  const int32_t* keep = a.keep_idx + (int64_t)b * a.K;
+  const int32_t* pt = a.pt + (int64_t)b * a.ld_pt;
+  int64_t* rec = a.offsets + 2 * (int64_t)b * a.K;
+  const bool side = a.scores || a.pos;
+  int bad = 0, hole = nk;
+  for (int j = tid; j < nk; j += kInplaceThreads) {
+    const int idx = keep[j];
+    const int prev = j > 0 ? keep[j - 1] : -1;
+    int64_t so = -1, dso = -1;
+    if (idx > prev && !(side && (int64_t)idx >= a.ld_s)) {
+      const int sp = idx / a.page_size;
+      const int dp = j / a.page_size;
+      if ((int64_t)sp < a.ld_pt) {  // dp <= sp since j <= idx
+        const int ps = pt[sp];
+        const int pd = pt[dp];
+        if (ps >= 0 && ps < a.n_pages && pd >= 0 && pd < a.n_pages) {
+          so = (int64_t)ps * a.s_page + (int64_t)(idx - sp * a.page_size) * a.row_bytes;
+          dso = (int64_t)pd * a.s_page + (int64_t)(j - dp * a.page_size) * a.row_bytes;
+        }
+      }
+    }
+    if (so < 0) bad = 1;
+    if (idx != j) hole = min(hole, j);
+    rec[2 * j] = so;
+    rec[2 * j + 1] = dso;
+  }
+  // block-wide "any bad" and "first hole"
+  bad = __any(bad);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) hole = min(hole, __shfl_xor(hole, m));
+  if (lane == 0) {
+    s_bad[wave] = bad;
+    s_hole[wave] = hole;
+  }
+  __syncthreads();
+  bad = 0;
+  hole = nk;
+  for (int w = 0; w < kInplaceThreads / 64; ++w) {
+    bad |= s_bad[w];
+    hole = min(hole, s_hole[w]);
+  }
+  if (bad) {
+    if (tid == 0) {
+      info[0] = info[1] = 0;
+      if (a.seq_status) a.seq_status[b] = EPIKV_SEQ_RANGE;
+    }
+    return;
+  }
+  if (tid == 0) {
+    info[0] = hole;
+    info[1] = nk;
+  }
+  if (!side) return;
+  // Scores and positions follow their rows, in ascending tiles (the same
+  // argument as the row move, with the workgroup barrier as the wait).
+  float* sc = a.scores ? a.scores + (int64_t)b * a.ld_s : nullptr;
+  int32_t* ps = a.pos ? a.pos + (int64_t)b * a.ld_s : nullptr;
+  for (int j0 = hole; j0 < nk; j0 += kInplaceThreads) {
+    const int j = j0 + tid;
+    float v = 0.f;
+    int32_t p = 0;
+    if (j < nk) {
+      const int idx = keep[j];
+      if (sc) v = sc[idx];
+      if (ps) p = ps[idx];
+    }
+    wait_vmem();
+    __syncthreads();
+    if (j < nk) {
+      if (sc) sc[j] = v;
+      if (ps) ps[j] = p;
+    }
+  }
+}
+
+template <int LPR, int NI>
+__global__ __launch_bounds__(kCompactThreads) void k_inplace_move(InplaceArgs a) {
+  constexpr int RPI = 64 / LPR;  // rows per load instruction
+  constexpr int T = RPI * NI;    // rows per tile
+  static_assert(T <= 64, "one record per lane");
+  const int lane = threadIdx.x & 63;
+  const int64_t unit = (int64_t)blockIdx.x * kCompactWaves + (threadIdx.x >> 6);
+  const int64_t per_seq = (int64_t)a.n_lk * a.n_slices;
+  const int b = (int)(unit / per_seq);
+  if (b >= a.B) return;
+  const int rem = (int)(unit - (int64_t)b * per_seq);
+  const int pl = rem / a.n_slices;
+  const int sl = rem - pl * a.n_slices;
+  const int h = a.info[2 * b];
+  const int nk = a.info[2 * b + 1];
+  if (h >= nk) return;
+  const int col = sl * LPR + lane % LPR;
+  const bool col_ok = col < (a.row_bytes >> 4);
+  const int rsub = lane / LPR;
+  char* base = a.pool + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + (int64_t)col * 16;
+  const int64_t* rec = a.offsets + 2 * (int64_t)b * a.K;
+  // lane i < T holds the record of the tile's row i
+  int64_t rs = -1, rd = -1;
+  if (lane < T && h + lane < nk) {
+    rs = rec[2 * (h + lane)];
+    rd = rec[2 * (h + lane) + 1];
+  }
+  // (waiting here too keeps the loop head free of a wait for the previous
+  // tile's stores)
+  wait_vmem();
+  for (int j0 = h; j0 < nk; j0 += T) {
+    u32x4 v[NI];
+    int64_t dd[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = i * RPI + rsub;
+      const int64_t s = shfl64(rs, t);
+      dd[i] = shfl64(rd, t);
+      if (s >= 0 && col_ok) v[i] = ld_stream(base + s);
+    }
+    // next tile's records, while this tile's rows are in flight
+    int64_t ns = -1, nd = -1;
+    const int jn = j0 + T + lane;
+    if (lane < T && jn < nk) {
+      ns = rec[2 * jn];
+      nd = rec[2 * jn + 1];
+    }
+    wait_vmem();
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      if (dd[i] >= 0 && col_ok) st_stream(base + dd[i], v[i]);
+    rs = ns;
+    rd = nd;
+  }
+}
+
+template <int LPR, int NI>
+hipError_t launch_move(const InplaceArgs& a, hipStream_t s) {
+  const int64_t units = (int64_t)a.B * a.n_lk * a.n_slices;
+  const int64_t blocks = (units + kCompactWaves - 1) / kCompactWaves;
+  hipLaunchKernelGGL((k_inplace_move<LPR, NI>), dim3((unsigned)blocks), dim3(kCompactThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_inplace_check, dim3(a.B), dim3(kInplaceThreads), 0, s, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (a.lanes_per_row == 64) return launch_move<64, 16>(a, s);
+  if (a.lanes_per_row == 16) return launch_move<16, 8>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace epikv

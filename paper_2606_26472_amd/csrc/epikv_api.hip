@@ -69,8 +69,13 @@ size_t sig_bytes(const epikv_cfg* c, int chunk) {
   return align_up(4 * (size_t)n_sig(c) * (size_t)c->batch * (size_t)chunk);
 }
 
-size_t compact_ws_bytes(const epikv_cfg* c) {
+// Row offset records [B][K][2] int64, then (in place) [B][2] int32.
+size_t compact_records_bytes(const epikv_cfg* c) {
   return align_up(16 * (size_t)c->batch * (size_t)c->budget);
+}
+
+size_t compact_ws_bytes(const epikv_cfg* c) {
+  return compact_records_bytes(c) + align_up(8 * (size_t)c->batch);
 }
 
 size_t partial_bytes(const epikv_cfg* c, int chunk) {
@@ -353,10 +358,65 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.n_lk = 2 * c->n_layers;
   // One wavefront per destination row, four rows and one (layer, K|V)
   // plane per workgroup: measured best on MI355X among 2..16 rows x 1..64
-  // planes for 32 sequences keeping 4096 of 8k..32k tokens.
+  // planes for 32 sequences keeping 4096 of 8k..32k tokens.  (A wavefront
+  // here has one 1 KiB load in flight at a time -- the compiler waits
+  // between the guarded loads; a branch-free variant with both loads in
+  // flight measured 5% slower, and more planes per wavefront slower still.)
   a.lk_per_block = 1;
   a.planes_together = 1;
   a.blocks_per_seq = (c->budget + kCompactWaves - 1) / kCompactWaves;
+  return a;
+}
+
+int check_compact_inplace(const epikv_cfg* c, const epikv_pool* pool, const int32_t* pt,
+                          int64_t ld_pt, const int32_t* keep_idx, const int32_t* n_keep,
+                          const float* scores, const int32_t* pos, int64_t ld_s, const void* ws,
+                          size_t ws_bytes) {
+  int st = check_cfg(c);
+  if (st) return st;
+  if (!ws || ws_bytes < compact_ws_bytes(c)) return EPIKV_EWORKSPACE;
+  if (!aligned16(ws)) return EPIKV_EALIGN;
+  st = check_pool(pool);
+  if (st) return st;
+  if (!pt || !keep_idx || !n_keep) return EPIKV_EINVAL_NULL;
+  if (ld_pt < 1) return EPIKV_EINVAL_SHAPE;
+  if ((scores || pos) && (ld_s < 1 || ld_s > INT32_MAX)) return EPIKV_EINVAL_SHAPE;
+  const size_t bytes = 4 * (size_t)c->batch * (size_t)(ld_s > 0 ? ld_s : 0);
+  if (scores && pos && overlap(scores, bytes, pos, bytes)) return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
+InplaceArgs inplace_args(const epikv_cfg* c, const epikv_pool* pool, const int32_t* pt,
+                         int64_t ld_pt, const int32_t* keep_idx, const int32_t* n_keep,
+                         float* scores, int32_t* pos, int64_t ld_s, int32_t* seq_status,
+                         void* ws) {
+  InplaceArgs a;
+  a.pool = (char*)pool->base;
+  a.s_layer = pool->stride_layer;
+  a.s_kv = pool->stride_kv;
+  a.s_page = pool->stride_page;
+  a.n_pages = pool->n_pages;
+  a.pt = pt;
+  a.ld_pt = ld_pt;
+  a.keep_idx = keep_idx;
+  a.n_keep = n_keep;
+  a.scores = scores;
+  a.pos = pos;
+  a.ld_s = ld_s;
+  a.seq_status = seq_status;
+  a.offsets = (int64_t*)ws;
+  a.info = (int32_t*)((char*)ws + compact_records_bytes(c));
+  a.B = c->batch;
+  a.K = c->budget;
+  a.page_size = c->page_size;
+  a.row_bytes = row_bytes(c);
+  a.n_lk = 2 * c->n_layers;
+  // A wavefront per (sequence, plane, 1 KiB column slice) when that gives
+  // enough independent walks; otherwise 256-byte slices (four rows per load).
+  const int row_vec = a.row_bytes / 16;
+  const int64_t wide = (int64_t)a.B * a.n_lk * ((row_vec + 63) / 64);
+  a.lanes_per_row = (row_vec >= 64 && wide >= kInplaceUnitsWanted) ? 64 : 16;
+  a.n_slices = (row_vec + a.lanes_per_row - 1) / a.lanes_per_row;
   return a;
 }
 
@@ -502,6 +562,20 @@ EPIKV_EXPORT int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src, cons
                                  stream));
 }
 
+EPIKV_EXPORT int epikv_compact_inplace(const epikv_cfg* cfg, const epikv_pool* pool,
+                                       const int32_t* page_table, int64_t ld_pt,
+                                       const int32_t* keep_idx, const int32_t* n_keep,
+                                       float* scores, int32_t* pos, int64_t ld_s,
+                                       int32_t* seq_status, void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
+  const int st = check_compact_inplace(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos,
+                                       ld_s, workspace, workspace_bytes);
+  if (st) return st;
+  return launched(launch_compact_inplace(inplace_args(cfg, pool, page_table, ld_pt, keep_idx, n_keep,
+                                                      scores, pos, ld_s, seq_status, workspace),
+                                         stream));
+}
+
 EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io, hipStream_t stream) {
   if (!io) return EPIKV_EINVAL_NULL;
   int st = check_cfg(cfg);
@@ -522,11 +596,20 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   if (st) return st;
   char* ws = (char*)io->workspace;
   char* ws_offsets = ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk);
-  // The scores are compacted only when the caller asks for them.
+  // The scores are compacted only when the caller asks for them (out of
+  // place); in place they always follow their rows.
   const float* src_scores = io->dst_scores ? io->scores : nullptr;
-  st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
-                     io->keep_idx, io->n_keep, src_scores, io->dst_scores, io->src_pos, io->dst_pos,
-                     io->ld_s, ws_offsets, compact_ws_bytes(cfg));
+  if (io->in_place) {
+    if (io->dst_scores && io->dst_scores != io->scores) return EPIKV_EALIAS;
+    if (io->src_pos != io->dst_pos) return EPIKV_EALIAS;
+    st = check_compact_inplace(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep,
+                               io->scores, io->dst_pos, io->ld_s, ws_offsets,
+                               compact_ws_bytes(cfg));
+  } else {
+    st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt,
+                       io->ld_dst_pt, io->keep_idx, io->n_keep, src_scores, io->dst_scores,
+                       io->src_pos, io->dst_pos, io->ld_s, ws_offsets, compact_ws_bytes(cfg));
+  }
   if (st) return st;
   const size_t ws_state = state_layout(cfg).total;
   if (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
@@ -546,6 +629,11 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                                           io->keep_idx, io->n_keep, io->seq_status, io->chunk),
                               stream));
   if (st) return st;
+  if (io->in_place)
+    return launched(launch_compact_inplace(
+        inplace_args(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep, io->scores,
+                     io->dst_pos, io->ld_s, io->seq_status, ws_offsets),
+        stream));
   return launched(launch_compact(
       compact_args(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
                    io->keep_idx, io->n_keep, src_scores, io->dst_scores,

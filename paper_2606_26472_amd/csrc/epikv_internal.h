@@ -117,6 +117,24 @@ struct CompactArgs {
   int32_t blocks_per_seq;                  // ceil(K / kCompactWaves)
 };
 
+struct InplaceArgs {
+  char* pool;
+  int64_t s_layer, s_kv, s_page, n_pages;
+  const int32_t* pt;                       // [B][ld_pt], source and destination
+  int64_t ld_pt;
+  const int32_t* keep_idx;                 // [B][K], strictly ascending
+  const int32_t* n_keep;
+  float* scores;                           // [B][ld_s], moved in place (optional)
+  int32_t* pos;                            // [B][ld_s], moved in place (optional)
+  int64_t ld_s;
+  int32_t* seq_status;                     // optional
+  int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
+  int32_t* info;                           // workspace [B][2]: first hole, rows kept
+  int32_t B, K, page_size, row_bytes, n_lk;
+  int32_t lanes_per_row;                   // 64 or 16 lanes share one row of a plane
+  int32_t n_slices;                        // ceil(row_bytes / 16 / lanes_per_row)
+};
+
 struct FillArgs {
   uint32_t* p;
   int64_t n_words;
@@ -132,16 +150,21 @@ hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r,
 hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
+hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s);
 hipError_t launch_fill(const FillArgs& a, hipStream_t s);
 
 // Tunables the host layer validates against.
 constexpr int kScoreThreads = 256;
-constexpr int kScoreSeg = 32;            // tokens per score_hs workgroup
+constexpr int kScoreSeg = 32;            // tokens per score_hs workgroup (wide rows)
+constexpr int kScoreSegWave = 32;        // longest segment per score_hs wavefront (rows <= 4096)
+constexpr int kScoreWavesWanted = 1024;  // shorten segments until this many wavefronts
 constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per lane)
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
 constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per gather workgroup
 constexpr int kLagMaxLds = 48 * 1024;
+constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
+constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
 
 }  // namespace epikv

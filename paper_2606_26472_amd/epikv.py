@@ -43,7 +43,7 @@ EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_workspace_bytes", "epikv_compact_workspace_bytes",
             "epikv_state_init", "epikv_score",
             "epikv_zscore", "epikv_select", "epikv_compact",
-            "epikv_evict_step")
+            "epikv_compact_inplace", "epikv_evict_step")
 
 
 class EpikvError(RuntimeError):
@@ -85,7 +85,8 @@ class StepIO(ctypes.Structure):
                 ("keep_idx", ctypes.c_void_p), ("n_keep", ctypes.c_void_p),
                 ("seq_status", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace_bytes", ctypes.c_size_t),
+                ("in_place", ctypes.c_int32)]
 
 
 _lib = None
@@ -120,6 +121,8 @@ def lib() -> ctypes.CDLL:
         "epikv_select": (ctypes.c_int, [cfgp, P, i64, P, P, P, P, P, P]),
         "epikv_compact": (ctypes.c_int, [cfgp, poolp, P, i64, poolp, P, i64,
                                          P, P, P, P, P, P, i64, P, P, sz, P]),
+        "epikv_compact_inplace": (ctypes.c_int, [cfgp, poolp, P, i64, P, P,
+                                                 P, P, i64, P, P, sz, P]),
         "epikv_evict_step": (ctypes.c_int, [cfgp, ctypes.POINTER(StepIO), P]),
     }
     for name, (res, args) in sig.items():
@@ -258,14 +261,30 @@ def epikv_compact(cfg: Cfg, src: Pool, src_pt, ld_src_pt, dst: Pool, dst_pt,
         "epikv_compact")
 
 
+def epikv_compact_inplace(cfg: Cfg, pool: Pool, page_table, ld_pt, keep_idx,
+                          n_keep, scores=None, pos=None, ld_s=0,
+                          seq_status=None, workspace=None, workspace_bytes_=0,
+                          stream=None):
+    _check(lib().epikv_compact_inplace(
+        ctypes.byref(cfg), ctypes.byref(pool), _ptr(page_table), int(ld_pt),
+        _ptr(keep_idx), _ptr(n_keep), _ptr(scores), _ptr(pos), int(ld_s),
+        _ptr(seq_status), _ptr(workspace), int(workspace_bytes_),
+        _stream(stream)), "epikv_compact_inplace")
+
+
 def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,
                  src: Pool, src_pt, ld_src_pt, dst: Pool, dst_pt, ld_dst_pt,
                  scores, ld_s, state_in, state_out, keep_idx, n_keep,
                  seq_status, workspace, workspace_bytes_, dst_scores=None,
-                 src_pos=None, dst_pos=None) -> StepIO:
-    """Build the epikv_step_io struct (keeps the hidden pointer array alive
-    on the returned object)."""
+                 src_pos=None, dst_pos=None, in_place=False) -> StepIO:
+    """Build the epikv_step_io struct.  The returned object holds references
+    to every tensor (and the hidden pointer array) it was built from, so a
+    temporary passed here cannot be freed while the struct is in use."""
     io = StepIO()
+    io._tensors_keepalive = [n_cached, n_prefix, src_pt, dst_pt, scores,
+                             state_in, state_out, keep_idx, n_keep,
+                             seq_status, workspace, dst_scores, src_pos,
+                             dst_pos, hidden]
     io.chunk = int(chunk)
     arr = _hidden_array(hidden)
     io._hidden_keepalive = arr
@@ -282,6 +301,7 @@ def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,
     io.keep_idx, io.n_keep = _ptr(keep_idx), _ptr(n_keep)
     io.seq_status = _ptr(seq_status)
     io.workspace, io.workspace_bytes = _ptr(workspace), int(workspace_bytes_)
+    io.in_place = 1 if in_place else 0
     return io
 
 

@@ -96,7 +96,7 @@ def test_state_layout_sizes(E):
     assert E.workspace_bytes(c, 128) >= 4 * 15 * 32 * 128
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
     assert E.workspace_bytes(c, 0) == 0
-    assert E.compact_workspace_bytes(c) == 16 * 32 * 4096
+    assert E.compact_workspace_bytes(c) == 16 * 32 * 4096 + 256
     assert E.workspace_bytes(c, 128) >= E.compact_workspace_bytes(c) \
         + 4 * 15 * 32 * 128
 
@@ -285,3 +285,50 @@ def test_evict_step_scores_copy_is_optional(E):
     io.workspace = io.state_in           # workspace overlapping the state
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EALIAS
+
+
+@host_only
+def test_compact_inplace_validation(E):
+    L = E.lib()
+    c = E.default_cfg(batch=2, budget=256)
+    f = L.epikv_compact_inplace
+    pool = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
+    bad = E.Pool(None, 0, 0, 0, 0)
+    W = 4 * A
+    n = E.compact_workspace_bytes(c)
+    assert n == 16 * 2 * 256 + 256       # records, then per-sequence info
+    assert f(ctypes.byref(c), ctypes.byref(bad), A, 4, A, A, None, None, 0,
+             None, W, n, None) == E.EPIKV_EINVAL_NULL
+    assert f(ctypes.byref(c), ctypes.byref(pool), None, 4, A, A, None, None,
+             0, None, W, n, None) == E.EPIKV_EINVAL_NULL
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, None, None, 0,
+             None, W, n - 1, None) == E.EPIKV_EWORKSPACE
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, None, None, 0,
+             None, W + 8, n, None) == E.EPIKV_EALIGN
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 0, A, A, None, None, 0,
+             None, W, n, None) == E.EPIKV_EINVAL_SHAPE      # ld_pt < 1
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, A, None, 0,
+             None, W, n, None) == E.EPIKV_EINVAL_SHAPE      # scores, ld_s 0
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, A, A + 64, 100,
+             None, W, n, None) == E.EPIKV_EALIAS            # scores on pos
+
+
+@host_only
+def test_evict_step_in_place_validation(E):
+    L = E.lib()
+    c = E.default_cfg(batch=2, budget=256)
+    io = _valid_io(E, A)
+    io.in_place = 1
+    io.dst_scores = 96 * A               # in place the scores move in place
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS
+    io = _valid_io(E, A)
+    io.in_place = 1
+    io.src_pos, io.dst_pos = 32 * A, 48 * A   # positions must be one array
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS
+    io = _valid_io(E, A)
+    io.in_place = 1
+    io.n_prefix = None                   # the earlier stages still check
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_NULL

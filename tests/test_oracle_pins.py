@@ -520,3 +520,67 @@ def test_compact_rows_bytewise():
     for j, i in enumerate(keep):
         assert out[j].tobytes() == rows[i].tobytes()
     assert out[2, 0, 0] == 0x7FC1
+
+
+# ---------------------------------------------------------------------------
+# App. H, in place (R18): pack the retained rows to the front of the
+# sequence's own pages
+# ---------------------------------------------------------------------------
+def _sequential_move(rows, keep):
+    """Independent check: move one row at a time, lowest slot first, in one
+    buffer, asserting that no source row is read after it was overwritten."""
+    buf = [r.copy() for r in rows]
+    written = np.zeros(len(rows), bool)
+    for j, i in enumerate(keep):
+        assert not written[i] or i == j, "source overwritten before its read"
+        buf[j] = buf[i].copy()
+        written[j] = True
+    return np.stack(buf)
+
+
+def test_inplace_rebuild_matches_sequential_move():
+    g = synth.rng(19)
+    for trial in range(200):
+        N = int(g.integers(1, 60))
+        rows = synth.random_bits16(g, (N, 3, 4))
+        if trial % 2:   # the real producer: the selection rule on scores
+            K = int(g.integers(1, N + 1))
+            P = int(g.integers(0, K))
+            keep = O.select_keep(g.standard_normal(N), P, K,
+                                 int(g.integers(0, K - P + 1)))
+            if isinstance(keep, str):
+                continue
+        else:           # any ascending subset
+            keep = np.sort(g.choice(N, int(g.integers(0, N + 1)),
+                                    replace=False))
+        out = O.compact_rows_inplace(rows, keep)
+        assert out.tobytes() == _sequential_move(rows, keep).tobytes()
+        n = len(keep)
+        assert out[:n].tobytes() == O.compact_rows(rows, keep).tobytes()
+        assert out[n:].tobytes() == rows[n:].tobytes()       # tail untouched
+        h = O.first_hole(keep)
+        assert out[:h].tobytes() == rows[:h].tobytes()       # leading run kept
+
+
+def test_inplace_rebuild_needs_ascending_order():
+    # moving the highest slot first overwrites a row before it is read, so
+    # the in-place form is only correct walked from the front
+    rows = np.arange(3, dtype=np.uint16)[:, None] * np.ones((1, 2), np.uint16)
+    keep = np.array([1, 2])
+    buf = rows.copy()
+    for j in reversed(range(keep.size)):
+        buf[j] = buf[keep[j]]
+    assert buf[0, 0] == 2                                    # wrong row
+    assert O.compact_rows_inplace(rows, keep)[0, 0] == 1     # the rebuild
+
+
+def test_first_hole():
+    assert O.first_hole(np.arange(5)) == 5
+    assert O.first_hole(np.array([0, 1, 3, 4])) == 2
+    assert O.first_hole(np.array([2, 3])) == 0
+    assert O.first_hole(np.array([], dtype=np.int64)) == 0
+    # protected prefill is never moved: the first hole is at or past P
+    g = synth.rng(20)
+    for _ in range(50):
+        keep = O.select_keep(g.standard_normal(300), 40, 100, 25)
+        assert O.first_hole(keep) >= 40
