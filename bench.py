@@ -182,6 +182,108 @@ def run_stages(E, S, w, events=None):
 
 
 # ---------------------------------------------------------------------------
+# In-place rebuild (epikv_compact_inplace) against the out-of-place one
+# ---------------------------------------------------------------------------
+def _time_calls(fn, reps, warm=3):
+    import torch
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    return float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
+
+
+def first_holes(keep, n_keep):
+    """Per sequence, the first slot whose retained position is not the slot
+    itself (n_keep when the kept set is a leading run): the in-place rebuild
+    moves exactly the slots from there to n_keep."""
+    out = []
+    for b in range(keep.shape[0]):
+        k = keep[b, :n_keep[b]]
+        bad = np.nonzero(k != np.arange(k.size))[0]
+        out.append(int(bad[0]) if bad.size else int(k.size))
+    return np.array(out)
+
+
+def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
+                        scores, dscores, ld_s, status, cws, reps):
+    """Time epikv_compact and epikv_compact_inplace on the same kept sets.
+    The in-place call rewrites the source pool: its later repetitions move
+    the same slots (the cost depends on the kept sets, not the bytes)."""
+    kh, nk = keep.cpu().numpy(), n_keep.cpu().numpy()
+    holes = first_holes(kh, nk)
+    row = w.kv_bytes_per_token
+    kept = int(nk.sum())
+    moved = int((nk - holes).sum())
+    ms_out = _time_calls(lambda: E.epikv_compact(
+        cfg, src, src_pt, src_pt.shape[1], dst, dst_pt, dst_pt.shape[1],
+        keep, n_keep, scores, dscores, None, None, ld_s, status, cws,
+        cws.numel()), reps)
+    ms_in = _time_calls(lambda: E.epikv_compact_inplace(
+        cfg, src, src_pt, src_pt.shape[1], keep, n_keep, scores, None, ld_s,
+        status, cws, cws.numel()), reps)
+    out_bytes = kept * (2 * row + 8)
+    in_bytes = moved * (2 * row + 8)
+    return {"rows_kept": kept, "rows_moved_in_place": moved,
+            "ms_out_of_place": round(ms_out, 4), "ms_in_place": round(ms_in, 4),
+            "gbps_out_of_place": round(out_bytes / ms_out / 1e6, 1),
+            "gbps_in_place": round(in_bytes / ms_in / 1e6, 1)}
+
+
+def inplace_report(E, S, w, reps):
+    import torch
+    dev = torch.device("cuda")
+    out = []
+    # 1. the headline batch (select already ran in the correctness guard)
+    r = compare_compactions(E, S.cfg, w, S.src, S.src_pt, S.dst, S.dst_pt,
+                            S.keep_idx, S.n_keep, S.scores, S.dst_scores,
+                            S.ld_s, S.status, S.cws, reps)
+    r["workload"] = (f"{w.name}: B={w.B}, N in [{w.n_min},{w.n_max}] -> "
+                     f"K={w.budget}, no protected prefill")
+    out.append(r)
+    log(f"[inplace] {r}")
+    del S.src_pool, S.dst_pool, S.src, S.dst
+    torch.cuda.empty_cache()
+    # 2. steady-state decode eviction: every sequence at K + C, back to K
+    B, K, C, page = w.B, w.budget, w.chunk, w.page_size
+    L, H, d = w.n_layers, w.n_kv_heads, w.head_dim
+    g = synth.rng(w.seed + 7)
+    lengths = np.full(B, K + C)
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.contiguous_page_tables(np.full(B, K), page)
+    src_pool = torch.empty((L, 2, n_src, page, H * d), dtype=torch.int16,
+                           device=dev)
+    src_pool.view(-1)[: 1 << 30].random_(-32768, 32768)
+    dst_pool = torch.zeros((L, 2, n_dst, page, H * d), dtype=torch.int16,
+                           device=dev)
+    src = E.pool_of(src_pool.view(L, 2, n_src, page, H, d))
+    dst = E.pool_of(dst_pool.view(L, 2, n_dst, page, H, d))
+    sc = np.stack([synth.old_scores(g, K + C) for _ in range(B)])
+    scores = torch.from_numpy(sc).to(dev)
+    dscores = torch.zeros_like(scores)
+    spt = torch.from_numpy(src_pt).to(dev)
+    dpt = torch.from_numpy(dst_pt).to(dev)
+    n_cached = torch.from_numpy(lengths.astype(np.int32)).to(dev)
+    for P in (0, 1024):
+        n_prefix = torch.full((B,), P, dtype=torch.int32, device=dev)
+        E.epikv_select(S.cfg, scores, K + C, n_cached, n_prefix, S.keep_idx,
+                       S.n_keep, S.status)
+        r = compare_compactions(E, S.cfg, w, src, spt, dst, dpt, S.keep_idx,
+                                S.n_keep, scores, dscores, K + C, S.status,
+                                S.cws, reps)
+        r["workload"] = (f"steady-state decode eviction: B={B}, N={K + C} "
+                         f"-> K={K}, protected prefill P={P}")
+        out.append(r)
+        log(f"[inplace] {r}")
+    return out
+
+
+# ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
 def cpu_baseline(w: synth.Workload, S, budget_s: float = 12.0):
@@ -288,6 +390,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stages-only", action="store_true",
                     help="only the per-stage loop (for profiling)")
+    ap.add_argument("--inplace", action="store_true",
+                    help="compare the in-place and out-of-place rebuilds "
+                         "(one JSON line of its own) instead of the step")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not "
@@ -316,6 +421,14 @@ def main():
     assert np.all(st == 0) and np.all(nk == np.minimum(S.lengths, w.budget)), \
         (st, nk)
     ab = algorithmic_bytes(w, S.lengths, nk)
+    if args.inplace:
+        rows = inplace_report(E, S, w, args.steps)
+        print(json.dumps({
+            "metric": "in-place vs out-of-place cache rebuild (GB/s of the "
+                      "bytes each must move)",
+            "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "data": "synthetic", "results": rows}), flush=True)
+        return
 
     stream = torch.cuda.current_stream()
     if not args.stages_only:

@@ -204,6 +204,7 @@ hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   if (a.lanes_per_row == 64) return launch_move<64, 16>(a, s);
   if (a.lanes_per_row == 16) return launch_move<16, 8>(a, s);
+  if (a.lanes_per_row == 4) return launch_move<4, 4>(a, s);
   return hipErrorInvalidValue;
 }
 

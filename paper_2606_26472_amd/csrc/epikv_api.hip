@@ -411,11 +411,19 @@ InplaceArgs inplace_args(const epikv_cfg* c, const epikv_pool* pool, const int32
   a.page_size = c->page_size;
   a.row_bytes = row_bytes(c);
   a.n_lk = 2 * c->n_layers;
-  // A wavefront per (sequence, plane, 1 KiB column slice) when that gives
-  // enough independent walks; otherwise 256-byte slices (four rows per load).
+  // A wavefront per (sequence, plane, column slice): the widest slice --
+  // 1 KiB, 256 B or 64 B, that is 64, 16 or 4 lanes per row -- that still
+  // gives enough independent walks to keep HBM busy (each walk has only
+  // one tile in flight).
   const int row_vec = a.row_bytes / 16;
-  const int64_t wide = (int64_t)a.B * a.n_lk * ((row_vec + 63) / 64);
-  a.lanes_per_row = (row_vec >= 64 && wide >= kInplaceUnitsWanted) ? 64 : 16;
+  a.lanes_per_row = 4;
+  for (int lpr = 64; lpr > 4; lpr /= 4) {
+    const int64_t units = (int64_t)a.B * a.n_lk * ((row_vec + lpr - 1) / lpr);
+    if (lpr <= row_vec && units >= kInplaceUnitsWanted) {
+      a.lanes_per_row = lpr;
+      break;
+    }
+  }
   a.n_slices = (row_vec + a.lanes_per_row - 1) / a.lanes_per_row;
   return a;
 }

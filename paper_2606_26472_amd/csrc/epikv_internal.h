@@ -131,7 +131,7 @@ struct InplaceArgs {
   int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
   int32_t* info;                           // workspace [B][2]: first hole, rows kept
   int32_t B, K, page_size, row_bytes, n_lk;
-  int32_t lanes_per_row;                   // 64 or 16 lanes share one row of a plane
+  int32_t lanes_per_row;                   // 64, 16 or 4 lanes share one row of a plane
   int32_t n_slices;                        // ceil(row_bytes / 16 / lanes_per_row)
 };
 

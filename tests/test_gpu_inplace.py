@@ -45,7 +45,11 @@ def _expected(pool, pt, keeps, lengths):
 
 CASES = {
     # name: overrides of _run
+    # column slices of 64 B, 256 B and 1 KiB (the library picks the widest
+    # that still gives 2048 independent walks)
     "narrow_slices": dict(lengths=[300, 90, 500], K=64),
+    "mid_slices": dict(lengths=[300, 90, 500, 120, 260, 64, 65, 200], K=64,
+                       L=16),
     "wide_slices": dict(lengths=list(range(64, 320, 8)), K=48, L=16),
     "page1": dict(lengths=[150, 90], K=40, page=1),
     "page1024": dict(lengths=[2500, 600], K=300, page=1024),
@@ -266,3 +270,52 @@ def test_inplace_step_small(E):
     assert np.array_equal(host(pos_d), exp_pos)
     exp_pool = _expected(pool, pt, keeps, lengths)
     assert host(pool_d).tobytes() == exp_pool.tobytes()
+
+
+def test_inplace_full_size_matches_out_of_place(E):
+    """The 32-sequence batch (N 8k..32k, K = 4096, 32 layers): the step run
+    out of place, then in place on the same inputs.  Every sequence's
+    scores and positions, and sampled rows of every layer and K/V, agree;
+    sampled slots past n_keep keep their bytes."""
+    import torch
+    import bench
+    print("in-place full size", flush=True)
+    w = synth.workload("ragged_batch32")
+    S = bench.setup_hs(w, E)
+    K, page = w.budget, w.page_size
+    E.epikv_evict_step(S.cfg, S.io)
+    torch.cuda.synchronize()
+    keep = host(S.keep_idx).copy()
+    assert np.all(host(S.status) == 0) and np.all(host(S.n_keep) == K)
+    g = synth.rng(902)
+    pick = {b: np.sort(g.choice(K, 32, replace=False)) for b in range(w.B)}
+    tail = {b: np.sort(g.choice(np.arange(K, int(S.lengths[b])), 16,
+                                replace=False)) for b in range(w.B)}
+
+    def rows(pool, pt, b, idx):
+        return host(pool[:, :, torch.from_numpy(
+            pt[b, idx // page].astype(np.int64)).cuda(),
+            torch.from_numpy((idx % page).astype(np.int64)).cuda(), :])
+
+    tail_before = {b: rows(S.src_pool, S.src_pt_host, b, tail[b])
+                   for b in range(w.B)}
+    io = E.make_step_io(
+        w.chunk, S.hidden_ptrs, w.hidden, w.chunk * w.hidden, S.n_cached,
+        S.n_prefix, S.src, S.src_pt, S.src_pt_host.shape[1], E.Pool(), None,
+        0, S.scores, S.ld_s, S.state_in, S.state_out, S.keep_idx, S.n_keep,
+        S.status, S.ws, S.ws_bytes, src_pos=S.src_pos, dst_pos=S.src_pos,
+        in_place=True)
+    E.epikv_evict_step(S.cfg, io)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(S.keep_idx), keep)
+    assert np.all(host(S.status) == 0)
+    assert host(S.scores)[:, :K].tobytes() == host(S.dst_scores)[:, :K].tobytes()
+    assert np.array_equal(host(S.src_pos)[:, :K], host(S.dst_pos)[:, :K])
+    moved = 0
+    for b in range(w.B):
+        moved += K - O.first_hole(keep[b])
+        assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, pick[b]),
+                              rows(S.dst_pool, S.dst_pt_host, b, pick[b])), b
+        assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, tail[b]),
+                              tail_before[b]), b
+    print(f"  rows moved: {moved} of {w.B * K}")
