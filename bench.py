@@ -198,6 +198,31 @@ def _time_calls(fn, reps, warm=3):
     return float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
 
 
+def _time_graph(fn, reps):
+    """Device time per call of `fn` with the host out of the loop: `reps`
+    calls captured in one HIP graph, replayed between two events."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    graph.replay()
+    ev[1].record()
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / reps
+
+
 def first_holes(keep, n_keep):
     """Per sequence, the first slot whose retained position is not the slot
     itself (n_keep when the kept set is a leading run): the in-place rebuild
@@ -280,6 +305,55 @@ def inplace_report(E, S, w, reps):
                          f"-> K={K}, protected prefill P={P}")
         out.append(r)
         log(f"[inplace] {r}")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Online scoring: one fused launch per decode token vs the two separate calls
+# ---------------------------------------------------------------------------
+def online_report(E, w, reps):
+    import torch
+    dev = torch.device("cuda")
+    B, D, nb = w.B, w.hidden, w.n_band
+    g = synth.rng(w.seed + 11)
+    out = []
+    for C in (1, 2, 4, 16, 64):
+        cfg = E.default_cfg(batch=B, hidden=D, n_band_a=len(w.band_a),
+                            n_band_b=len(w.band_b), window=w.window)
+        hid = torch.from_numpy(synth.f32_to_bf16_bits(
+            g.standard_normal((nb, B, C, D), dtype=np.float32)).view(
+                np.int16)).to(dev)
+        hidden = [hid[l] for l in range(nb)]
+        st = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8)
+        sec = E.state_sections(cfg, st)
+        sec["n_tok"][:] = 5000
+        sec["ring"][:] = torch.from_numpy(
+            (50 + g.standard_normal(tuple(sec["ring"].shape))).astype(
+                np.float32))
+        st_in = st.to(dev)
+        st_out = torch.zeros_like(st_in)
+        ld_s = 8192
+        scores = torch.zeros((B, ld_s), device=dev)
+        n_cached = torch.full((B,), 5000 + C, dtype=torch.int32, device=dev)
+        sig = torch.zeros((nb, B, C), device=dev)
+
+        def two():
+            E.epikv_score(cfg, C, hidden, D, C * D, state_in=st_in,
+                          state_out=st_out, sig=sig)
+            E.epikv_zscore(cfg, C, sig, n_cached, st_in, st_out, scores, ld_s)
+
+        def fused():
+            E.epikv_score_tokens(cfg, C, hidden, D, C * D, n_cached, st_in,
+                                 st_out, scores, ld_s)
+
+        ms2 = _time_graph(two, reps)
+        ms1 = _time_graph(fused, reps)
+        by = B * nb * (C + 2) * D * 2          # rows + h_prev in/out
+        r = {"tokens_per_call": C, "B": B, "us_fused": round(ms1 * 1e3, 2),
+             "us_two_calls": round(ms2 * 1e3, 2),
+             "gbps_fused": round(by / ms1 / 1e6, 1)}
+        log(f"[online] {r}")
+        out.append(r)
     return out
 
 
@@ -390,6 +464,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stages-only", action="store_true",
                     help="only the per-stage loop (for profiling)")
+    ap.add_argument("--online", action="store_true",
+                    help="time the fused per-token scorer against the two "
+                         "separate calls (one JSON line of its own)")
     ap.add_argument("--inplace", action="store_true",
                     help="compare the in-place and out-of-place rebuilds "
                          "(one JSON line of its own) instead of the step")
@@ -411,6 +488,14 @@ def main():
         print("only hidden-state workloads are benchmarked", file=sys.stderr)
         sys.exit(2)
     log(f"[bench] workload {w.name}: B={w.B} K={w.budget} C={w.chunk}")
+    if args.online:
+        rows = online_report(E, w, max(args.steps, 100))
+        print(json.dumps({
+            "metric": "online scoring: microseconds per scoring call "
+                      "(hidden-state signal, 15 band layers x 4096)",
+            "unit": "us", "n_gpus": 1, "data": "synthetic",
+            "results": rows}), flush=True)
+        return
     S = setup_hs(w, E)
 
     # correctness guard: one step, every sequence must be OK with K kept

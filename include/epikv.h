@@ -243,6 +243,27 @@ int epikv_zscore(const epikv_cfg* cfg, int32_t chunk, const float* sig,
                  float* smoothed, hipStream_t stream);
 
 /*
+ * epikv_score_tokens -- epikv_score and epikv_zscore in one launch, for the
+ * online regime of Sec. 3.3: a decoder scores each token (or a few) as it
+ * is generated and freezes the score; an eviction then needs only
+ * epikv_select + epikv_compact.
+ *
+ * Hidden-state signal only (cfg->signal == EPIKV_SIGNAL_HS), every
+ * smoothing mode, 1 <= chunk <= 64, cfg->hidden <= 4096.  Arguments as for
+ * epikv_score (hidden, ld_tok, ld_seq, state_in, state_out) and
+ * epikv_zscore (n_cached, scores, ld_s); no signal buffer or workspace (the
+ * signal stays on chip).  The scores written and the state_out produced are
+ * bit for bit those of the two separate calls.  Errors: EINVAL_PARAM for
+ * another signal, EINVAL_SHAPE for chunk or hidden out of range, and the
+ * checks of epikv_score / epikv_zscore.
+ */
+int epikv_score_tokens(const epikv_cfg* cfg, int32_t chunk,
+                       const void* const* hidden, int64_t ld_tok,
+                       int64_t ld_seq, const int32_t* n_cached,
+                       const void* state_in, void* state_out, float* scores,
+                       int64_t ld_s, hipStream_t stream);
+
+/*
  * epikv_select -- positions that survive (Sec. 3.1, Sec. 3.3, App. D).
  *
  * Per sequence with N = n_cached[b] and P = n_prefix[b]:

@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libepikv.so")
 
 SOURCES = ["epikv_api.hip", "score_hs.hip", "score_lagkv.hip", "zscore.hip",
-           "select.hip", "compact.hip", "compact_inplace.hip"]
+           "select.hip", "compact.hip", "compact_inplace.hip", "score_tokens.hip"]
 
 ARCH = "gfx950"
 CXXFLAGS = [

@@ -229,6 +229,55 @@ int run_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int6
   return launched(launch_score_lagkv(a, r, s));
 }
 
+int check_score_tokens(const epikv_cfg* c, int32_t chunk, const void* const* hidden,
+                       int64_t ld_tok, int64_t ld_seq, const int32_t* n_cached,
+                       const void* state_in, void* state_out, float* scores, int64_t ld_s) {
+  int st = check_cfg(c);
+  if (st) return st;
+  if (c->signal != EPIKV_SIGNAL_HS) return EPIKV_EINVAL_PARAM;
+  if (chunk < 1 || chunk > kZscoreTile || c->hidden > kTokMaxRow) return EPIKV_EINVAL_SHAPE;
+  if (!n_cached || !scores) return EPIKV_EINVAL_NULL;
+  if (ld_s < chunk) return EPIKV_EINVAL_SHAPE;
+  // the hidden-state and state checks of epikv_score (no signal buffer: it
+  // stays on chip)
+  return check_score(c, chunk, hidden, ld_tok, ld_seq, nullptr, nullptr, 0, n_cached, state_in,
+                     state_out, scores, nullptr, 0, false);
+}
+
+ScoreTokArgs score_tokens_args(const epikv_cfg* c, int32_t chunk, const void* const* hidden,
+                               int64_t ld_tok, int64_t ld_seq, const int32_t* n_cached,
+                               const void* state_in, void* state_out, float* scores,
+                               int64_t ld_s) {
+  const Layout L = state_layout(c);
+  ScoreTokArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int l = 0; l < n_band(c); ++l) a.hidden[l] = (const uint16_t*)hidden[l];
+  a.ld_tok = ld_tok;
+  a.ld_seq = ld_seq;
+  a.B = c->batch;
+  a.C = chunk;
+  a.D = c->hidden;
+  a.n_band = n_band(c);
+  a.n_a = c->n_band_a;
+  a.n_b = c->n_band_b;
+  a.w = c->window;
+  a.mode = c->smoothing;
+  a.eps = c->eps;
+  a.alpha = c->ema_alpha;
+  a.n_cached = n_cached;
+  a.n_tok_in = (const int32_t*)state_in;
+  a.ring_in = (const float*)((const char*)state_in + L.off[1]);
+  a.h_prev_in = (const uint16_t*)((const char*)state_in + L.off[2]);
+  a.ema_in = (const float*)((const char*)state_in + L.off[4]);
+  a.n_tok_out = (int32_t*)state_out;
+  a.ring_out = (float*)((char*)state_out + L.off[1]);
+  a.h_prev_out = (uint16_t*)((char*)state_out + L.off[2]);
+  a.ema_out = (float*)((char*)state_out + L.off[4]);
+  a.scores = scores;
+  a.ld_s = ld_s;
+  return a;
+}
+
 int check_zscore(const epikv_cfg* c, int32_t chunk, const float* sig, const int32_t* n_cached,
                  const void* state_in, void* state_out, float* scores, int64_t ld_s) {
   int st = check_cfg(c);
@@ -543,6 +592,18 @@ EPIKV_EXPORT int epikv_zscore(const epikv_cfg* cfg, int32_t chunk, const float* 
   if (st) return st;
   return launched(launch_zscore(
       zscore_args(cfg, chunk, sig, n_cached, state_in, state_out, scores, ld_s, smoothed), stream));
+}
+
+EPIKV_EXPORT int epikv_score_tokens(const epikv_cfg* cfg, int32_t chunk, const void* const* hidden,
+                                    int64_t ld_tok, int64_t ld_seq, const int32_t* n_cached,
+                                    const void* state_in, void* state_out, float* scores,
+                                    int64_t ld_s, hipStream_t stream) {
+  const int st = check_score_tokens(cfg, chunk, hidden, ld_tok, ld_seq, n_cached, state_in,
+                                    state_out, scores, ld_s);
+  if (st) return st;
+  return launched(launch_score_tokens(score_tokens_args(cfg, chunk, hidden, ld_tok, ld_seq, n_cached,
+                                                        state_in, state_out, scores, ld_s),
+                                      stream));
 }
 
 EPIKV_EXPORT int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t ld_s,

@@ -43,6 +43,26 @@ struct ScoreHsArgs {
   float* sig;                              // [n_band][B][C]
 };
 
+// Fused per-token scoring (Eq. 1 + smoothing + band combination) of chunks of
+// at most kZscoreTile tokens with rows of at most 4096 elements.
+struct ScoreTokArgs {
+  const uint16_t* hidden[EPIKV_MAX_BAND];
+  int64_t ld_tok, ld_seq;
+  int32_t B, C, D, n_band, n_a, n_b, w, mode;
+  float eps, alpha;
+  const int32_t* n_cached;
+  const int32_t* n_tok_in;
+  const float* ring_in;
+  const uint16_t* h_prev_in;
+  const float* ema_in;
+  int32_t* n_tok_out;
+  float* ring_out;
+  uint16_t* h_prev_out;
+  float* ema_out;
+  float* scores;
+  int64_t ld_s;
+};
+
 struct ScoreLagArgs {
   const char* base;                        // pool
   int64_t s_layer, s_kv, s_page, n_pages;
@@ -142,9 +162,78 @@ struct FillArgs {
 };
 
 // ---------------------------------------------------------------------------
+// Arithmetic shared by kernels that must agree bit for bit (the fused
+// per-token scorer and the separate score / zscore kernels)
+// ---------------------------------------------------------------------------
+// Accumulate the squared differences of eight bf16 pairs (Eq. 1), in order.
+__device__ __forceinline__ float sqdiff8(u32x4 a, u32x4 b, float acc) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float d0 = bf16_lo(a[k]) - bf16_lo(b[k]);
+    const float d1 = bf16_hi(a[k]) - bf16_hi(b[k]);
+    acc = fmaf(d0, d0, acc);
+    acc = fmaf(d1, d1, acc);
+  }
+  return acc;
+}
+
+// Smoothed value of the sample at extended index j over its window [lo, j]
+// (Eq. 3 z-score, Eq. 2 mean, or the raw sample); x holds the extended
+// samples from index `base` on.  Two passes over at most w values.
+__device__ __forceinline__ float smooth_at(const float* x, int base, int lo, int j, int mode,
+                                           float eps) {
+  const float n = (float)(j - lo + 1);
+  const float xv = x[j - base];
+  if (mode == EPIKV_SMOOTH_RAW) return xv;
+  float s = 0.f;
+  for (int k = lo; k <= j; ++k) s += x[k - base];
+  const float mu = s / n;
+  if (mode == EPIKV_SMOOTH_MEAN) return mu;
+  float q = 0.f;
+  for (int k = lo; k <= j; ++k) {
+    const float dlt = x[k - base] - mu;
+    q = fmaf(dlt, dlt, q);
+  }
+  return (xv - mu) / (sqrtf(q / n) + eps);
+}
+
+// EMA over one 64-token tile of a signal row (App. E): each lane's token is
+// the affine map y -> A*y + Bc (the identity without a sample, y = x at the
+// stream's first sample); an inclusive lane scan composes them and applies
+// the result to the average carried into the tile.
+__device__ __forceinline__ float ema_scan(float x, bool has, bool first, float al, float bl,
+                                          float carry, int lane) {
+  float A = has ? (first ? 0.f : al) : 1.f;
+  float Bc = has ? (first ? x : bl * x) : 0.f;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float pa = __shfl_up(A, off, 64);
+    const float pb = __shfl_up(Bc, off, 64);
+    if (lane >= off) {
+      Bc = fmaf(A, pb, Bc);
+      A = A * pa;
+    }
+  }
+  return fmaf(A, carry, Bc);
+}
+
+// s = mean over Band A rows - mean over Band B rows of token t (Fig. 1).
+template <int TILE>
+__device__ __forceinline__ float band_combine(const float (*vals)[TILE], int t, int n_a,
+                                              int n_sig, int n_b) {
+  float sa = 0.f, sb = 0.f;
+  for (int l = 0; l < n_a; ++l) sa += vals[l][t];
+  for (int l = n_a; l < n_sig; ++l) sb += vals[l][t];
+  float s = sa / (float)n_a;
+  if (n_b > 0) s -= sb / (float)n_b;
+  return s;
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (return the HIP error of the launch; never synchronise)
 // ---------------------------------------------------------------------------
 hipError_t launch_score_hs(const ScoreHsArgs& a, hipStream_t s);
+hipError_t launch_score_tokens(const ScoreTokArgs& a, hipStream_t s);
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r,
                               hipStream_t s);
 hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s);
@@ -160,6 +249,7 @@ constexpr int kScoreSegWave = 32;        // longest segment per score_hs wavefro
 constexpr int kScoreWavesWanted = 1024;  // shorten segments until this many wavefronts
 constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per lane)
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
+constexpr int kTokMaxRow = 4096;         // fused per-token scorer: widest hidden row
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
 constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per gather workgroup

@@ -17,17 +17,6 @@
 namespace epikv {
 namespace {
 
-__device__ __forceinline__ float sqdiff8(u32x4 a, u32x4 b, float acc) {
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const float d0 = bf16_lo(a[k]) - bf16_lo(b[k]);
-    const float d1 = bf16_hi(a[k]) - bf16_hi(b[k]);
-    acc = fmaf(d0, d0, acc);
-    acc = fmaf(d1, d1, acc);
-  }
-  return acc;
-}
-
 template <int VPT, int U>
 __global__ __launch_bounds__(kScoreThreads) void k_score_hs(ScoreHsArgs a) {
   __shared__ float red[kScoreThreads / 64][U];

@@ -73,26 +73,7 @@ __global__ __launch_bounds__(kZscoreThreads) void k_zscore(ZscoreArgs a) {
       float v = 0.f;
       if (c < a.C && c >= c0) {
         const int j = wm1 + c;
-        const int lo = max(vstart, j - wm1);
-        const float n = (float)(j - lo + 1);
-        const float xv = x[j - base];
-        if (a.mode == EPIKV_SMOOTH_RAW) {
-          v = xv;
-        } else {
-          float s = 0.f;
-          for (int k = lo; k <= j; ++k) s += x[k - base];
-          const float mu = s / n;
-          if (a.mode == EPIKV_SMOOTH_MEAN) {
-            v = mu;
-          } else {
-            float q = 0.f;
-            for (int k = lo; k <= j; ++k) {
-              const float dlt = x[k - base] - mu;
-              q = fmaf(dlt, dlt, q);
-            }
-            v = (xv - mu) / (sqrtf(q / n) + a.eps);
-          }
-        }
+        v = smooth_at(x, base, max(vstart, j - wm1), j, a.mode, a.eps);
       }
       vals[l][lane] = v;
       if (a.smoothed && c < a.C) a.smoothed[((int64_t)l * a.B + b) * a.C + c] = v;
@@ -110,11 +91,7 @@ __global__ __launch_bounds__(kZscoreThreads) void k_zscore(ZscoreArgs a) {
   }
 
   if (tid < kZscoreTile && c < a.C) {
-    float sa = 0.f, sb = 0.f;
-    for (int l = 0; l < a.n_a; ++l) sa += vals[l][tid];
-    for (int l = a.n_a; l < a.n_sig; ++l) sb += vals[l][tid];
-    float s = sa / (float)a.n_a;
-    if (a.n_b > 0) s -= sb / (float)a.n_b;
+    const float s = band_combine<kZscoreTile>(vals, tid, a.n_a, a.n_sig, a.n_b);
     const int N = a.n_cached[b];
     if (N >= a.C && (int64_t)N <= a.ld_s) a.scores[(int64_t)b * a.ld_s + (N - a.C) + c] = s;
   }
@@ -157,18 +134,7 @@ __global__ __launch_bounds__(kZscoreThreads) void k_ema(ZscoreArgs a) {
       const int l = rd * kZscoreWaves + wave;
       if (l < a.n_sig) {
         const float x = has ? a.sig[((int64_t)l * a.B + b) * a.C + c] : 0.f;
-        float A = has ? (first ? 0.f : al) : 1.f;
-        float Bc = has ? (first ? x : bl * x) : 0.f;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const float pa = __shfl_up(A, off, 64);
-          const float pb = __shfl_up(Bc, off, 64);
-          if (lane >= off) {
-            Bc = fmaf(A, pb, Bc);
-            A = A * pa;
-          }
-        }
-        const float y = fmaf(A, carry[l], Bc);
+        const float y = ema_scan(x, has, first, al, bl, carry[l], lane);
         const float v = has ? y : 0.f;
         vals[l][lane] = v;
         if (a.smoothed && c < a.C) a.smoothed[((int64_t)l * a.B + b) * a.C + c] = v;
@@ -177,14 +143,9 @@ __global__ __launch_bounds__(kZscoreThreads) void k_ema(ZscoreArgs a) {
       }
     }
     __syncthreads();
-    if (tid < kZscoreTile && c < a.C && write_scores) {
-      float sa = 0.f, sb = 0.f;
-      for (int l = 0; l < a.n_a; ++l) sa += vals[l][tid];
-      for (int l = a.n_a; l < a.n_sig; ++l) sb += vals[l][tid];
-      float s = sa / (float)a.n_a;
-      if (a.n_b > 0) s -= sb / (float)a.n_b;
-      a.scores[(int64_t)b * a.ld_s + (N - a.C) + c] = s;
-    }
+    if (tid < kZscoreTile && c < a.C && write_scores)
+      a.scores[(int64_t)b * a.ld_s + (N - a.C) + c] =
+          band_combine<kZscoreTile>(vals, tid, a.n_a, a.n_sig, a.n_b);
     __syncthreads();
   }
   // carried state: averages, sample ring, token count

@@ -41,7 +41,7 @@ MAX_BAND = 32
 EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_state_bytes", "epikv_state_layout",
             "epikv_workspace_bytes", "epikv_compact_workspace_bytes",
-            "epikv_state_init", "epikv_score",
+            "epikv_state_init", "epikv_score", "epikv_score_tokens",
             "epikv_zscore", "epikv_select", "epikv_compact",
             "epikv_compact_inplace", "epikv_evict_step")
 
@@ -118,6 +118,8 @@ def lib() -> ctypes.CDLL:
         "epikv_score": (ctypes.c_int, [cfgp, i32, ctypes.POINTER(P), i64, i64,
                                        poolp, P, i64, P, P, P, P, P, sz, P]),
         "epikv_zscore": (ctypes.c_int, [cfgp, i32, P, P, P, P, P, i64, P, P]),
+        "epikv_score_tokens": (ctypes.c_int, [cfgp, i32, ctypes.POINTER(P), i64,
+                                              i64, P, P, P, P, i64, P]),
         "epikv_select": (ctypes.c_int, [cfgp, P, i64, P, P, P, P, P, P]),
         "epikv_compact": (ctypes.c_int, [cfgp, poolp, P, i64, poolp, P, i64,
                                          P, P, P, P, P, P, i64, P, P, sz, P]),
@@ -237,6 +239,15 @@ def epikv_zscore(cfg: Cfg, chunk: int, sig, n_cached, state_in, state_out,
         ctypes.byref(cfg), int(chunk), _ptr(sig), _ptr(n_cached),
         _ptr(state_in), _ptr(state_out), _ptr(scores), int(ld_s),
         _ptr(smoothed), _stream(stream)), "epikv_zscore")
+
+
+def epikv_score_tokens(cfg: Cfg, chunk: int, hidden, ld_tok, ld_seq, n_cached,
+                       state_in, state_out, scores, ld_s, stream=None):
+    arr = _hidden_array(hidden)
+    _check(lib().epikv_score_tokens(
+        ctypes.byref(cfg), int(chunk), arr, int(ld_tok), int(ld_seq),
+        _ptr(n_cached), _ptr(state_in), _ptr(state_out), _ptr(scores),
+        int(ld_s), _stream(stream)), "epikv_score_tokens")
 
 
 def epikv_select(cfg: Cfg, scores, ld_s, n_cached, n_prefix, keep_idx,

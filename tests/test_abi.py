@@ -332,3 +332,23 @@ def test_evict_step_in_place_validation(E):
     io.n_prefix = None                   # the earlier stages still check
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EINVAL_NULL
+
+
+@host_only
+def test_score_tokens_validation(E):
+    L = E.lib()
+    f = L.epikv_score_tokens
+    c = E.default_cfg(batch=2, n_band_a=1, n_band_b=1)
+    hid = (ctypes.c_void_p * 2)(A, A + 4096)
+    ok = (ctypes.byref(c), 1, hid, 4096, 4096, A, 8 * A, 9 * A, 10 * A, 100,
+          None)
+    lag = E.default_cfg(batch=2, signal=E.SIGNAL_LAGKV)
+    assert f(ctypes.byref(lag), *ok[1:]) == E.EPIKV_EINVAL_PARAM
+    assert f(ok[0], 65, *ok[2:]) == E.EPIKV_EINVAL_SHAPE        # chunk > 64
+    assert f(ok[0], 0, *ok[2:]) == E.EPIKV_EINVAL_SHAPE
+    wide = E.default_cfg(batch=2, n_band_a=1, n_band_b=1, hidden=8192)
+    assert f(ctypes.byref(wide), *ok[1:]) == E.EPIKV_EINVAL_SHAPE
+    assert f(*ok[:8], None, *ok[9:]) == E.EPIKV_EINVAL_NULL      # no scores
+    assert f(*ok[:5], None, *ok[6:]) == E.EPIKV_EINVAL_NULL      # no n_cached
+    assert f(*ok[:9], 0, None) == E.EPIKV_EINVAL_SHAPE           # ld_s < chunk
+    assert f(*ok[:7], 8 * A, *ok[8:]) == E.EPIKV_EALIAS          # state in place

@@ -27,25 +27,33 @@ def E():
     return epikv
 
 
-def _score_stream(E, cfg, hid, chunks):
-    """Score a [n_band][B][T][D] stream cut into the given chunk sizes;
-    returns (scores [B][T], final state bytes)."""
+def _score_stream(E, cfg, hid, chunks, fused=False, state0=None):
+    """Score a [n_band][B][T][D] stream cut into the given chunk sizes, with
+    epikv_score + epikv_zscore or (fused) epikv_score_tokens; returns
+    (scores [B][T], final state bytes)."""
     import torch
     nb, B, T, D = hid.shape
     hd = dev(hid)
     st = [torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
           for _ in range(2)]
-    E.epikv_state_init(cfg, st[0])
+    if state0 is None:
+        E.epikv_state_init(cfg, st[0])
+    else:
+        st[0].copy_(state0)
     scores = torch.zeros((B, T), device="cuda")
     t0 = 0
     for C in chunks:
-        sig = torch.zeros((nb, B, C), device="cuda")
         # rows t0..t0+C-1 of every sequence: [nb][B][T][D] with ld_seq = T*D
         hidden = [hd[l, :, t0:] for l in range(nb)]
-        E.epikv_score(cfg, C, hidden, D, T * D, state_in=st[0],
-                      state_out=st[1], sig=sig)
         n_cached = dev(np.full(B, t0 + C, np.int32))
-        E.epikv_zscore(cfg, C, sig, n_cached, st[0], st[1], scores, T)
+        if fused:
+            E.epikv_score_tokens(cfg, C, hidden, D, T * D, n_cached, st[0],
+                                 st[1], scores, T)
+        else:
+            sig = torch.zeros((nb, B, C), device="cuda")
+            E.epikv_score(cfg, C, hidden, D, T * D, state_in=st[0],
+                          state_out=st[1], sig=sig)
+            E.epikv_zscore(cfg, C, sig, n_cached, st[0], st[1], scores, T)
         st = [st[1], st[0]]
         t0 += C
     assert t0 == T
@@ -108,3 +116,39 @@ def test_ema_online_matches_one_shot(E):
         s64 = O.band_score(np.array(sm), na, nb)
         assert np.max(np.abs(s1[b] - s64) / np.maximum(1.0, np.abs(s64))) \
             <= 1e-3
+
+
+@pytest.mark.parametrize("mode", ["z", "mean", "raw", "ema"])
+@pytest.mark.parametrize("D", [1000, 4096])
+def test_score_tokens_equals_two_calls(E, mode, D):
+    """epikv_score_tokens (one launch per call) against epikv_score +
+    epikv_zscore on the same chunking: scores and carried state bitwise,
+    from a fresh stream and from a carried state (window 64 and 5)."""
+    import torch
+    print(f"fused per-token scoring {mode} D={D}", flush=True)
+    g = synth.rng(903 + D)
+    B, T = 3, 150
+    w = synth.workload("drift_replay", B=B, hidden=D)
+    na, nb = len(w.band_a), len(w.band_b)
+    hid = np.stack([np.stack([synth.hidden_rows(
+        synth.amplitudes(w, g, 0, T)[l], D, g) for b in range(B)])
+        for l in range(w.n_band)])
+    smode = {"z": E.SMOOTH_Z, "mean": E.SMOOTH_MEAN, "raw": E.SMOOTH_RAW,
+             "ema": E.SMOOTH_EMA}[mode]
+    for window in (64, 5):
+        cfg = E.default_cfg(batch=B, hidden=D, n_band_a=na, n_band_b=nb,
+                            smoothing=smode, window=window)
+        # a carried state: the stream's first 40 tokens scored beforehand
+        _, st40 = _score_stream(E, cfg, hid[:, :, :40], [40])
+        for chunks in ([1] * 12 + [7, 64, 1, 2, 64], [64, 64, 22]):
+            a = _score_stream(E, cfg, hid, chunks)
+            f = _score_stream(E, cfg, hid, chunks, fused=True)
+            assert a[0].tobytes() == f[0].tobytes(), (window, chunks)
+            assert a[1].tobytes() == f[1].tobytes(), (window, chunks)
+        rest = hid[:, :, 40:]
+        a = _score_stream(E, cfg, rest, [1] * 20 + [30, 60],
+                          state0=torch.from_numpy(st40).cuda())
+        f = _score_stream(E, cfg, rest, [1] * 20 + [30, 60], fused=True,
+                          state0=torch.from_numpy(st40).cuda())
+        assert a[0].tobytes() == f[0].tobytes()
+        assert a[1].tobytes() == f[1].tobytes()
