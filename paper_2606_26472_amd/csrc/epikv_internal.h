@@ -185,11 +185,15 @@ __device__ __forceinline__ float smooth_at(const float* x, int base, int lo, int
   const float n = (float)(j - lo + 1);
   const float xv = x[j - base];
   if (mode == EPIKV_SMOOTH_RAW) return xv;
+  // (unrolled so that the LDS reads issue ahead of the additions, which
+  // stay in order)
   float s = 0.f;
+#pragma unroll 8
   for (int k = lo; k <= j; ++k) s += x[k - base];
   const float mu = s / n;
   if (mode == EPIKV_SMOOTH_MEAN) return mu;
   float q = 0.f;
+#pragma unroll 8
   for (int k = lo; k <= j; ++k) {
     const float dlt = x[k - base] - mu;
     q = fmaf(dlt, dlt, q);
