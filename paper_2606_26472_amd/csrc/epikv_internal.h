@@ -257,6 +257,9 @@ constexpr int kTokMaxRow = 4096;         // fused per-token scorer: widest hidde
 constexpr int kSelectThreads = 1024;
 constexpr int kCompactThreads = 256;
 constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per gather workgroup
+// Dynamic LDS the gather reserves (and never touches) to cap it at six
+// workgroups per CU: 160 KiB of LDS per CU on gfx950 / 24 KiB = 6.
+constexpr int kCompactLdsCap = 24 * 1024;
 constexpr int kLagMaxLds = 48 * 1024;
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
