@@ -63,12 +63,18 @@ def _oracle_stream_scores(hid_all, na, nb, w=64, eps=1e-6):
 # ---------------------------------------------------------------------------
 # Multi-step replay of one stream
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("name,steps,min_evict,row_sample", [
-    ("drift_replay", 16, 12, None), ("spike_replay", 40, 8, 256)])
-def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
+@pytest.mark.parametrize("name,steps,min_evict,row_sample,P,bands", [
+    ("drift_replay", 16, 12, None, 0, "bands"),
+    ("drift_replay", 16, 12, None, 64, "10/21"),
+    ("spike_replay", 40, 8, 256, 0, "bands"),
+    ("spike_replay", 40, 8, 256, 64, "bands")])
+def test_replay_matches_oracle(E, name, steps, min_evict, row_sample, P,
+                               bands):
+    """P: protected prefill tokens; bands: the 7-13 / 18-25 bands, or the
+    single-layer preset A = {10}, B = {21} (Eq. 3's z_10 - z_21)."""
     import torch
     w = synth.workload(name)
-    print(f"replay {name} steps={steps}", flush=True)
+    print(f"replay {name} steps={steps} P={P} {bands}", flush=True)
     g = synth.rng(w.seed)
     C, K, page = w.chunk, w.budget, w.page_size
     L, H, d, D = w.n_layers, w.n_kv_heads, w.head_dim, w.hidden
@@ -79,6 +85,12 @@ def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
     hid_all = np.empty((w.n_band, T, D), dtype=np.uint16)
     for l in range(w.n_band):
         hid_all[l] = synth.hidden_rows(a[l], D, g)
+    if bands == "10/21":
+        rows = [list(w.band_a).index(10),
+                len(w.band_a) + list(w.band_b).index(21)]
+        hid_all = np.ascontiguousarray(hid_all[rows])
+        na, nb = 1, 1
+    n_band = na + nb
     kv_tok = synth.random_bits16(g, (T, L, 2, H * d))
     s_ref = _oracle_stream_scores(hid_all, na, nb, w.window)
 
@@ -102,7 +114,7 @@ def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
     keep = torch.zeros((1, K), dtype=torch.int32, device="cuda")
     n_keep = torch.zeros(1, dtype=torch.int32, device="cuda")
     status = torch.zeros(1, dtype=torch.int32, device="cuda")
-    n_prefix = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n_prefix = torch.full((1,), P, dtype=torch.int32, device="cuda")
     cache_tok = np.zeros(0, dtype=np.int64)     # token ids held, in order
     x = 0                                        # pool holding the cache
     R = O.default_recent(K)
@@ -122,7 +134,7 @@ def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
         pos[x][0, n_prev:N] = torch.from_numpy(new_tok.astype(np.int32)).cuda()
         hid = dev(np.ascontiguousarray(hid_all[:, None, t0:t0 + C, :]))
         io = E.make_step_io(
-            C, [hid[l] for l in range(w.n_band)], D, C * D,
+            C, [hid[l] for l in range(n_band)], D, C * D,
             dev(np.array([N], np.int32)), n_prefix,
             E.pool_of(pools[x].view(L, 2, n_pages, page, H, d)), pts[x],
             n_pages, E.pool_of(pools[1 - x].view(L, 2, n_pages, page, H, d)),
@@ -139,13 +151,14 @@ def test_replay_matches_oracle(E, name, steps, min_evict, row_sample):
         assert _rel_err(gpu_scores[n_prev:], s_ref[new_tok]) <= TOL, step
         kidx = host(keep)[0, :nk]
         # same-precision decision: the oracle ranking the GPU's fp32 scores
-        ref32 = O.select_keep(gpu_scores, 0, K, R)
+        ref32 = O.select_keep(gpu_scores, P, K, R)
         assert np.array_equal(kidx, ref32), step
         # against the oracle's own fp64 scores, with the near-tie exemption
-        ref64 = O.select_keep(s_ref[all_tok], 0, K, R)
+        ref64 = O.select_keep(s_ref[all_tok], P, K, R)
         if N > K:
-            swaps += tie_exempt_compare(kidx, ref64, s_ref[all_tok], 0, N,
+            swaps += tie_exempt_compare(kidx, ref64, s_ref[all_tok], P, N,
                                         K, R)
+            assert np.array_equal(kidx[:P], np.arange(P))  # prefill kept
         if N > K:
             evictions += 1
         # the rebuilt cache: token ids, scores and every row bit-exact
