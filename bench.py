@@ -427,12 +427,11 @@ def copy_ceiling(n_bytes: int = 4 << 30, reps: int = 5):
     return 2 * n_bytes / (ms * 1e-3) / 1e9, float(ms)
 
 
-COMPACT_SOURCES = ("paper_2606_26472_amd/csrc/compact.hip",
-                   "paper_2606_26472_amd/csrc/epikv_api.hip")
+COMPACT_SOURCES = ("paper_2606_26472_amd/csrc/compact.hip",)
 
 
 def compact_source_hash() -> str:
-    """Hash of the sources that define the compaction kernels and their
+    """Hash of the source that defines the compaction kernels and their
     launch shape."""
     h = hashlib.sha256()
     for rel in COMPACT_SOURCES:

@@ -129,6 +129,31 @@ int launched(hipError_t e) { return e == hipSuccess ? EPIKV_OK : EPIKV_ELAUNCH; 
 // ---------------------------------------------------------------------------
 // Per-stage validation + argument building
 // ---------------------------------------------------------------------------
+// The state pair: both present, aligned, and not overlapping (a step reads
+// the whole input state after writing parts of the output).
+int check_state_pair(const epikv_cfg* c, const void* state_in, void* state_out) {
+  if (!state_in || !state_out) return EPIKV_EINVAL_NULL;
+  if (!aligned16(state_in) || !aligned16(state_out)) return EPIKV_EALIGN;
+  const size_t sb = state_layout(c).total;
+  if (overlap(state_in, sb, state_out, sb)) return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
+// The band-layer hidden states of a chunk: one aligned pointer per band
+// layer, rows of D elements at ld_tok, sequences at ld_seq.
+int check_hidden(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,
+                 int64_t ld_seq) {
+  if (!hidden) return EPIKV_EINVAL_NULL;
+  for (int l = 0; l < n_band(c); ++l) {
+    if (!hidden[l]) return EPIKV_EINVAL_NULL;
+    if (!aligned16(hidden[l])) return EPIKV_EALIGN;
+  }
+  if (ld_tok < 0 || ld_seq < 0) return EPIKV_EINVAL_SHAPE;
+  if (chunk > 1 && ld_tok < c->hidden) return EPIKV_EINVAL_SHAPE;
+  if ((ld_tok % 8) || (ld_seq % 8)) return EPIKV_EALIGN;
+  return EPIKV_OK;
+}
+
 int check_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,
                 int64_t ld_seq, const epikv_pool* pool, const int32_t* page_table, int64_t ld_pt,
                 const int32_t* n_cached, const void* state_in, void* state_out, float* sig,
@@ -137,18 +162,11 @@ int check_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, in
   if (st) return st;
   if (!state_in || !state_out || !sig) return EPIKV_EINVAL_NULL;
   if (chunk < 1) return EPIKV_EINVAL_SHAPE;
-  if (!aligned16(state_in) || !aligned16(state_out)) return EPIKV_EALIGN;
-  const size_t sb = state_layout(c).total;
-  if (overlap(state_in, sb, state_out, sb)) return EPIKV_EALIAS;
+  st = check_state_pair(c, state_in, state_out);
+  if (st) return st;
   if (c->signal == EPIKV_SIGNAL_HS) {
-    if (!hidden) return EPIKV_EINVAL_NULL;
-    for (int l = 0; l < n_band(c); ++l) {
-      if (!hidden[l]) return EPIKV_EINVAL_NULL;
-      if (!aligned16(hidden[l])) return EPIKV_EALIGN;
-    }
-    if (ld_tok < 0 || ld_seq < 0) return EPIKV_EINVAL_SHAPE;
-    if (chunk > 1 && ld_tok < c->hidden) return EPIKV_EINVAL_SHAPE;
-    if ((ld_tok % 8) || (ld_seq % 8)) return EPIKV_EALIGN;
+    st = check_hidden(c, chunk, hidden, ld_tok, ld_seq);
+    if (st) return st;
   } else {
     st = check_pool(pool);
     if (st) return st;
@@ -236,12 +254,11 @@ int check_score_tokens(const epikv_cfg* c, int32_t chunk, const void* const* hid
   if (st) return st;
   if (c->signal != EPIKV_SIGNAL_HS) return EPIKV_EINVAL_PARAM;
   if (chunk < 1 || chunk > kZscoreTile || c->hidden > kTokMaxRow) return EPIKV_EINVAL_SHAPE;
-  if (!n_cached || !scores) return EPIKV_EINVAL_NULL;
+  if (!n_cached || !scores || !state_in || !state_out) return EPIKV_EINVAL_NULL;
   if (ld_s < chunk) return EPIKV_EINVAL_SHAPE;
-  // the hidden-state and state checks of epikv_score (no signal buffer: it
-  // stays on chip)
-  return check_score(c, chunk, hidden, ld_tok, ld_seq, nullptr, nullptr, 0, n_cached, state_in,
-                     state_out, scores, nullptr, 0, false);
+  st = check_state_pair(c, state_in, state_out);
+  if (st) return st;
+  return check_hidden(c, chunk, hidden, ld_tok, ld_seq);
 }
 
 ScoreTokArgs score_tokens_args(const epikv_cfg* c, int32_t chunk, const void* const* hidden,
@@ -405,15 +422,6 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.page_size = c->page_size;
   a.row_bytes = row_bytes(c);
   a.n_lk = 2 * c->n_layers;
-  // One wavefront per destination row, four rows and one (layer, K|V)
-  // plane per workgroup: measured best on MI355X among 2..16 rows x 1..64
-  // planes for 32 sequences keeping 4096 of 8k..32k tokens.  (A wavefront
-  // here has one 1 KiB load in flight at a time -- the compiler waits
-  // between the guarded loads; a branch-free variant with both loads in
-  // flight measured 5% slower, and more planes per wavefront slower still.)
-  a.lk_per_block = 1;
-  a.planes_together = 1;
-  a.blocks_per_seq = (c->budget + kCompactWaves - 1) / kCompactWaves;
   return a;
 }
 

@@ -132,6 +132,7 @@ struct CompactArgs {
   int32_t* seq_status;                     // optional
   int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
   int32_t B, K, page_size, row_bytes, n_lk;
+  // launch shape, chosen by launch_compact
   int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
   int32_t planes_together;                 // planes loaded before storing (1,2,4,8)
   int32_t blocks_per_seq;                  // ceil(K / kCompactWaves)
