@@ -262,6 +262,7 @@ constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per ga
 // workgroups per CU: 160 KiB of LDS per CU on gfx950 / 24 KiB = 6.
 constexpr int kCompactLdsCap = 24 * 1024;
 constexpr int kLagMaxLds = 48 * 1024;
+constexpr int kLagRowsAhead = 8;         // chunk rows a Lag-KV thread loads before using them
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
 

@@ -13,18 +13,40 @@
 // Kernel 1: one 256-thread workgroup per (layer, K|V) plane and sequence
 // streams the chunk's rows of that plane from the paged pool (planes of an
 // unused tensor only zero their partial sums).  Thread i owns
-// 8 channels (one 16-byte column) of a row; the d/8 lanes of one head reduce
-// the variance with butterfly shuffles (two passes: mean, then squared
-// deviations), and per-(token, head) variances go to LDS.  The workgroup
-// then writes per-token sums over its heads to partial[b][plane][c].
+// 8 channels (one 16-byte column) of a row and loads kLagRowsAhead rows
+// (page-table entries first, then the rows) before using any; the d/8 lanes
+// of one head reduce the variance with DPP row operations (two passes: mean,
+// then squared deviations), and per-(token, head) variances go to LDS.  The
+// normalisation multiplies by the reciprocal of the channel's range.  The
+// workgroup then writes per-token sums over its heads to
+// partial[b][plane][c].
 // Kernel 2 sums the 2L planes in a fixed order and divides by L*H.
 #include "epikv_internal.h"
 
 namespace epikv {
 namespace {
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of `width` lanes (8, 16 or 32), every lane of a
+// group ending with the same bits: each step adds two values that the
+// partner lane adds in the other order.  DPP moves within a row of 16 lanes
+// (rotations, half-row mirror, quad permutes) instead of LDS shuffles.
 __device__ __forceinline__ float group_sum(float v, int width) {
-  for (int off = width >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if (width == 8) {
+    v += dpp<0x141>(v);  // row_half_mirror: lane i + lane 7-i
+    v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+    return v;
+  }
+  v += dpp<0x128>(v);    // row_ror:8
+  v += dpp<0x124>(v);    // row_ror:4
+  v += dpp<0x122>(v);    // row_ror:2
+  v += dpp<0x121>(v);    // row_ror:1
+  if (width == 32) v += __shfl_xor(v, 16, 64);
   return v;
 }
 
@@ -69,12 +91,16 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
   const bool fresh = a.lag && a.n_tok_in[b] <= 0;
 
-  // Address of this thread's column of chunk row r, or nullptr.
-  auto row_ptr = [&](int r) -> const char* {
-    if (!seq_ok) return nullptr;
-    const int pos = start + r;
-    const int pg = pt[pos / a.page_size];
+  // Page of chunk row r (-1 for none), then the address of this thread's
+  // column of the row (nullptr for none).  Split so that a batch of rows
+  // issues all its page-table loads before any row load waits on one.
+  auto row_page = [&](int r) -> int {
+    if (!seq_ok || r >= a.C) return -1;
+    return pt[(start + r) / a.page_size];
+  };
+  auto row_ptr = [&](int r, int pg) -> const char* {
     if (pg < 0 || pg >= a.n_pages) return nullptr;
+    const int pos = start + r;
     return plane + (int64_t)pg * a.s_page + (int64_t)(pos % a.page_size) * row_bytes + col * 16;
   };
 
@@ -109,15 +135,28 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   };
 
   if (fresh) {
-    for (int r = ro; r < a.C && ro < rpp; r += rpp) {
-      const char* p = row_ptr(r);
-      if (!p) continue;
-      float x[8];
-      unpack8(ld_stream(p), x);
+    for (int r0 = ro; r0 < a.C && ro < rpp; r0 += kLagRowsAhead * rpp) {
+      u32x4 raw[kLagRowsAhead];
+      bool got[kLagRowsAhead];
+      int pg[kLagRowsAhead];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        cmn[e] = fminf(cmn[e], x[e]);
-        cmx[e] = fmaxf(cmx[e], x[e]);
+      for (int u = 0; u < kLagRowsAhead; ++u) pg[u] = row_page(r0 + u * rpp);
+#pragma unroll
+      for (int u = 0; u < kLagRowsAhead; ++u) {
+        const char* p = row_ptr(r0 + u * rpp, pg[u]);
+        got[u] = p != nullptr;
+        if (got[u]) raw[u] = ld_stream(p);
+      }
+#pragma unroll
+      for (int u = 0; u < kLagRowsAhead; ++u) {
+        if (!got[u]) continue;
+        float x[8];
+        unpack8(raw[u], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          cmn[e] = fminf(cmn[e], x[e]);
+          cmx[e] = fmaxf(cmx[e], x[e]);
+        }
       }
     }
     combine();
@@ -141,41 +180,59 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   }
   float den[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) den[e] = mx[e] - mn[e] + a.eps;
+  for (int e = 0; e < 8; ++e) den[e] = 1.0f / (mx[e] - mn[e] + a.eps);
 
   const float inv_d = 1.0f / (float)a.d;
   // All threads run the same trip count so that the head-group shuffles see
   // every lane of the group.
+  // kLagRowsAhead rows per thread are loaded before any is used, so each
+  // thread has that many 16-byte loads in flight.
   const int trips = (a.C + rpp - 1) / rpp;
-  for (int it = 0; it < trips; ++it) {
-    const int r = it * rpp + ro;
-    const bool live = ro < rpp && r < a.C;
-    const char* p = live ? row_ptr(r) : nullptr;
-    float x[8];
-    if (p) {
-      unpack8(ld_stream(p), x);
+  for (int it0 = 0; it0 < trips; it0 += kLagRowsAhead) {
+    u32x4 raw[kLagRowsAhead];
+    bool got[kLagRowsAhead];
+    int pg[kLagRowsAhead];
+#pragma unroll
+    for (int u = 0; u < kLagRowsAhead; ++u) {
+      const int r = (it0 + u) * rpp + ro;
+      pg[u] = ro < rpp ? row_page(r) : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kLagRowsAhead; ++u) {
+      const char* p = row_ptr((it0 + u) * rpp + ro, pg[u]);
+      got[u] = p != nullptr;
+      if (got[u]) raw[u] = ld_stream(p);
+    }
+#pragma unroll
+    for (int u = 0; u < kLagRowsAhead; ++u) {
+      const int r = (it0 + u) * rpp + ro;
+      const bool live = ro < rpp && r < a.C && it0 + u < trips;
+      float x[8];
+      if (got[u]) {
+        unpack8(raw[u], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          cmn[e] = fminf(cmn[e], x[e]);
+          cmx[e] = fmaxf(cmx[e], x[e]);
+          if (a.lag) x[e] = (x[e] - mn[e]) * den[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = 0.f;
+      }
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += x[e];
+      const float mu = group_sum(s, gl) * inv_d;
+      float q = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        cmn[e] = fminf(cmn[e], x[e]);
-        cmx[e] = fmaxf(cmx[e], x[e]);
-        if (a.lag) x[e] = (x[e] - mn[e]) / den[e];
+        const float dlt = x[e] - mu;
+        q = fmaf(dlt, dlt, q);
       }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = 0.f;
+      const float var = group_sum(q, gl) * inv_d;
+      if (live && (col % gl) == 0) vbuf[r * a.H + head] = got[u] ? var : 0.f;
     }
-    float s = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) s += x[e];
-    const float mu = group_sum(s, gl) * inv_d;
-    float q = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float dlt = x[e] - mu;
-      q = fmaf(dlt, dlt, q);
-    }
-    const float var = group_sum(q, gl) * inv_d;
-    if (live && (col % gl) == 0) vbuf[r * a.H + head] = p ? var : 0.f;
   }
   __syncthreads();
   if (a.lag) {
