@@ -2,6 +2,8 @@
 // launches.  Every host-detectable error is returned before anything is
 // enqueued; nothing here allocates, synchronises or keeps global state.
 #include <math.h>
+
+#include <algorithm>
 #include <string.h>
 
 #include "epikv_internal.h"
@@ -78,9 +80,28 @@ size_t compact_ws_bytes(const epikv_cfg* c) {
   return compact_records_bytes(c) + align_up(8 * (size_t)c->batch);
 }
 
+// Workgroups sharing the rows of one (plane, sequence) in the KV-vector
+// scorer: enough for about kLagWgWanted workgroups, each keeping at least
+// kLagRowsAhead rows per thread.
+int lag_splits(const epikv_cfg* c, int chunk) {
+  const int rpp = kScoreThreads / (c->n_kv_heads * c->head_dim / 8);
+  const int64_t base = 2 * (int64_t)c->n_layers * c->batch;
+  int64_t s = (kLagWgWanted + base - 1) / base;
+  const int64_t cap = std::max<int64_t>(1, chunk / (rpp * kLagRowsAhead));
+  return (int)std::max<int64_t>(1, std::min(s, cap));
+}
+
+size_t prange_bytes(const epikv_cfg* c, int chunk) {
+  if (!uses_range(c->signal)) return 0;
+  return align_up(4 * (size_t)lag_splits(c, chunk) * 2 * (size_t)c->batch * (size_t)c->n_layers *
+                  2 * (size_t)c->n_kv_heads * (size_t)c->head_dim);
+}
+
+// Per-plane partial sums, then the per-split partial channel ranges.
 size_t partial_bytes(const epikv_cfg* c, int chunk) {
   if (!is_kv(c->signal)) return 0;
-  return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk);
+  return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk) +
+         prange_bytes(c, chunk);
 }
 
 int check_cfg(const epikv_cfg* c) {
@@ -227,12 +248,23 @@ void lag_args(const epikv_cfg* c, int32_t chunk, const epikv_pool* pool, const i
   a->range_in = (const float*)((const char*)state_in + L.off[3]);
   a->range_out = (float*)((char*)state_out + L.off[3]);
   a->partial = partial;
+  a->splits = lag_splits(c, chunk);
+  a->prange = a->lag ? (float*)((char*)partial + align_up(4 * (size_t)c->batch * 2 *
+                                                          (size_t)c->n_layers * (size_t)chunk))
+                     : nullptr;
   r->partial = partial;
   r->sig = sig;
   r->B = c->batch;
   r->C = chunk;
   r->n_lk = 2 * c->n_layers;
   r->inv_count = 1.0f / (float)(c->n_layers * c->n_kv_heads);
+  r->lag = a->lag;
+  r->use_k = a->use_k;
+  r->use_v = a->use_v;
+  r->splits = a->splits;
+  r->n_chan = c->n_layers * 2 * c->n_kv_heads * c->head_dim;
+  r->prange = a->prange;
+  r->range_out = a->range_out;
 }
 
 int run_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, int64_t ld_tok,

@@ -76,6 +76,8 @@ struct ScoreLagArgs {
   const float* range_in;                   // [2][B][L][2][H][d] (lag only)
   float* range_out;
   float* partial;                          // [B][2L][C]
+  int32_t splits;                          // workgroups sharing one plane's rows
+  float* prange;                           // [splits][2][B][L][2][H][d] partial ranges
 };
 
 struct LagReduceArgs {
@@ -83,6 +85,9 @@ struct LagReduceArgs {
   float* sig;                              // [B][C]
   int32_t B, C, n_lk;
   float inv_count;                         // 1 / (L*H)
+  int32_t lag, use_k, use_v, splits, n_chan;  // n_chan = L*2*H*d channels per sequence
+  const float* prange;
+  float* range_out;                        // [2][B][L][2][H][d]
 };
 
 struct ZscoreArgs {
@@ -263,6 +268,7 @@ constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per ga
 constexpr int kCompactLdsCap = 24 * 1024;
 constexpr int kLagMaxLds = 48 * 1024;
 constexpr int kLagRowsAhead = 8;         // chunk rows a Lag-KV thread loads before using them
+constexpr int kLagWgWanted = 1024;       // split a plane's rows until this many workgroups
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
 

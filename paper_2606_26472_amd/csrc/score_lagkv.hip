@@ -10,9 +10,10 @@
 // out as the next chunk's reference; the first chunk of a stream, with no
 // previous chunk, is normalised by its own range.
 //
-// Kernel 1: one 256-thread workgroup per (layer, K|V) plane and sequence
-// streams the chunk's rows of that plane from the paged pool (planes of an
-// unused tensor only zero their partial sums).  Thread i owns
+// Kernel 1: 256-thread workgroups per (layer, K|V) plane and sequence, each
+// streaming its share of the chunk's rows of that plane from the paged pool
+// (planes of an unused tensor only zero their partial sums; the first chunk
+// of a stream goes to one workgroup, which needs every row for the range).  Thread i owns
 // 8 channels (one 16-byte column) of a row and loads kLagRowsAhead rows
 // (page-table entries first, then the rows) before using any; the d/8 lanes
 // of one head reduce the variance with DPP row operations (two passes: mean,
@@ -20,7 +21,8 @@
 // normalisation multiplies by the reciprocal of the channel's range.  The
 // workgroup then writes per-token sums over its heads to
 // partial[b][plane][c].
-// Kernel 2 sums the 2L planes in a fixed order and divides by L*H.
+// Kernel 2 sums the 2L planes in a fixed order and divides by L*H, and
+// combines the shares' channel ranges into the next chunk's reference.
 #include "epikv_internal.h"
 
 namespace epikv {
@@ -63,6 +65,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int tid = threadIdx.x;
   const int lk = blockIdx.x;
   const int b = blockIdx.y;
+  const int sp = blockIdx.z;                   // which share of the chunk's rows
   const int layer = lk >> 1;
   const int kv = lk & 1;
   const int HD = a.H * a.d;
@@ -78,7 +81,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   float* cmb = lds + a.C * a.H;                // [2][rpp][HD] range combine
   float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
   if ((kv == 0 && !a.use_k) || (kv == 1 && !a.use_v)) {
-    for (int r = tid; r < a.C; r += kScoreThreads) part[r] = 0.f;
+    if (sp == 0)
+      for (int r = tid; r < a.C; r += kScoreThreads) part[r] = 0.f;
     return;
   }
 
@@ -90,12 +94,23 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int64_t half = (int64_t)a.B * a.L * 2 * HD;
   const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
   const bool fresh = a.lag && a.n_tok_in[b] <= 0;
+  // Rows [r_lo, r_hi) of the chunk are this workgroup's.  The first chunk of
+  // a stream is normalised by its own range, which needs every row before
+  // any variance: one workgroup takes it whole.
+  int r_lo = 0, r_hi = 0;
+  if (fresh) {
+    r_hi = sp == 0 ? a.C : 0;
+  } else {
+    const int per = ((a.C + a.splits - 1) / a.splits + rpp - 1) / rpp * rpp;
+    r_lo = min(a.C, sp * per);
+    r_hi = min(a.C, r_lo + per);
+  }
 
   // Page of chunk row r (-1 for none), then the address of this thread's
   // column of the row (nullptr for none).  Split so that a batch of rows
   // issues all its page-table loads before any row load waits on one.
   auto row_page = [&](int r) -> int {
-    if (!seq_ok || r >= a.C) return -1;
+    if (!seq_ok || r >= r_hi) return -1;
     return pt[(start + r) / a.page_size];
   };
   auto row_ptr = [&](int r, int pg) -> const char* {
@@ -135,7 +150,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   };
 
   if (fresh) {
-    for (int r0 = ro; r0 < a.C && ro < rpp; r0 += kLagRowsAhead * rpp) {
+    for (int r0 = r_lo + ro; r0 < r_hi && ro < rpp; r0 += kLagRowsAhead * rpp) {
       u32x4 raw[kLagRowsAhead];
       bool got[kLagRowsAhead];
       int pg[kLagRowsAhead];
@@ -187,26 +202,26 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   // every lane of the group.
   // kLagRowsAhead rows per thread are loaded before any is used, so each
   // thread has that many 16-byte loads in flight.
-  const int trips = (a.C + rpp - 1) / rpp;
+  const int trips = (r_hi - r_lo + rpp - 1) / rpp;
   for (int it0 = 0; it0 < trips; it0 += kLagRowsAhead) {
     u32x4 raw[kLagRowsAhead];
     bool got[kLagRowsAhead];
     int pg[kLagRowsAhead];
 #pragma unroll
     for (int u = 0; u < kLagRowsAhead; ++u) {
-      const int r = (it0 + u) * rpp + ro;
+      const int r = r_lo + (it0 + u) * rpp + ro;
       pg[u] = ro < rpp ? row_page(r) : -1;
     }
 #pragma unroll
     for (int u = 0; u < kLagRowsAhead; ++u) {
-      const char* p = row_ptr((it0 + u) * rpp + ro, pg[u]);
+      const char* p = row_ptr(r_lo + (it0 + u) * rpp + ro, pg[u]);
       got[u] = p != nullptr;
       if (got[u]) raw[u] = ld_stream(p);
     }
 #pragma unroll
     for (int u = 0; u < kLagRowsAhead; ++u) {
-      const int r = (it0 + u) * rpp + ro;
-      const bool live = ro < rpp && r < a.C && it0 + u < trips;
+      const int r = r_lo + (it0 + u) * rpp + ro;
+      const bool live = ro < rpp && r < r_hi;
       float x[8];
       if (got[u]) {
         unpack8(raw[u], x);
@@ -236,30 +251,57 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   }
   __syncthreads();
   if (a.lag) {
+    // this share's range of the chunk; the reduce kernel combines the shares
     combine();
     if (ro == 0) {
+      float* pr = a.prange + (int64_t)sp * 2 * half;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        a.range_out[rbase + e] = cmn[e];
-        a.range_out[half + rbase + e] = cmx[e];
+        pr[rbase + e] = cmn[e];
+        pr[half + rbase + e] = cmx[e];
       }
     }
   }
-  for (int r = tid; r < a.C; r += kScoreThreads) {
+  for (int r = r_lo + tid; r < r_hi; r += kScoreThreads) {
     float s = 0.f;
     for (int h = 0; h < a.H; ++h) s += vbuf[r * a.H + h];
     part[r] = s;
   }
 }
 
+// Blocks [0, tok_blocks) of each sequence: q(t) = the 2L plane sums of
+// token t in a fixed order, times 1/(L*H).  The remaining blocks (lag
+// signals): each channel's range over the chunk = the min and max of the
+// shares' partial ranges, in a fixed order.
 __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
-  const int c = blockIdx.x * kScoreThreads + threadIdx.x;
   const int b = blockIdx.y;
-  if (c >= a.C) return;
-  const float* p = a.partial + (int64_t)b * a.n_lk * a.C + c;
-  float s = 0.f;
-  for (int lk = 0; lk < a.n_lk; ++lk) s += p[(int64_t)lk * a.C];
-  a.sig[(int64_t)b * a.C + c] = s * a.inv_count;
+  const int tok_blocks = (a.C + kScoreThreads - 1) / kScoreThreads;
+  if ((int)blockIdx.x < tok_blocks) {
+    const int c = blockIdx.x * kScoreThreads + threadIdx.x;
+    if (c >= a.C) return;
+    const float* p = a.partial + (int64_t)b * a.n_lk * a.C + c;
+    float s = 0.f;
+#pragma unroll 8
+    for (int lk = 0; lk < a.n_lk; ++lk) s += p[(int64_t)lk * a.C];
+    a.sig[(int64_t)b * a.C + c] = s * a.inv_count;
+    return;
+  }
+  const int i = ((int)blockIdx.x - tok_blocks) * kScoreThreads + threadIdx.x;
+  if (i >= a.n_chan) return;
+  const int64_t half = (int64_t)a.B * a.n_chan;
+  const int64_t o = (int64_t)b * a.n_chan + i;
+  const int kv = (i / (a.n_chan / a.n_lk)) & 1;
+  float lo = 0.f, hi = 0.f;  // planes of an unused tensor carry no range
+  if (kv == 0 ? a.use_k : a.use_v) {
+    lo = a.prange[o];
+    hi = a.prange[half + o];
+    for (int sp = 1; sp < a.splits; ++sp) {
+      lo = fminf(lo, a.prange[sp * 2 * half + o]);
+      hi = fmaxf(hi, a.prange[sp * 2 * half + half + o]);
+    }
+  }
+  a.range_out[o] = lo;
+  a.range_out[half + o] = hi;
 }
 
 }  // namespace
@@ -272,11 +314,13 @@ size_t lagkv_lds_bytes(int C, int H, int d) {
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
   const size_t lds = lagkv_lds_bytes(a.C, a.H, a.d);
-  hipLaunchKernelGGL(k_score_lagkv, dim3(2 * a.L, a.B), dim3(kScoreThreads), lds, s, a);
+  hipLaunchKernelGGL(k_score_lagkv, dim3(2 * a.L, a.B, a.splits), dim3(kScoreThreads), lds, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_lag_reduce, dim3((r.C + kScoreThreads - 1) / kScoreThreads, r.B),
-                     dim3(kScoreThreads), 0, s, r);
+  const int tok_blocks = (r.C + kScoreThreads - 1) / kScoreThreads;
+  const int rng_blocks = r.lag ? (r.n_chan + kScoreThreads - 1) / kScoreThreads : 0;
+  hipLaunchKernelGGL(k_lag_reduce, dim3(tok_blocks + rng_blocks, r.B), dim3(kScoreThreads), 0, s,
+                     r);
   return hipGetLastError();
 }
 
