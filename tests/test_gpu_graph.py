@@ -112,3 +112,92 @@ def test_graph_replays_match_eager(E, signal):
             assert a.tobytes() == b.tobytes(), rep    # bytewise: NaN-safe
         junk = junk * 1.0001 + 1.0              # unrelated eager work
         torch.cuda.synchronize()
+
+
+def test_graph_in_place_step_and_token_scorer(E):
+    """The in-place step and the fused per-token scorer under capture: each
+    replay starts from the same inputs (the pool, scores and positions the
+    in-place step rewrites are restored first) and must match eager."""
+    import torch
+    print("graph capture in place + score_tokens", flush=True)
+    g = synth.rng(801)
+    B, C, K, page, L, H, d, D = 3, 16, 96, 16, 2, 8, 128, 256
+    na, nb = 2, 2
+    lengths = np.array([400, 150, 90])
+    ld_s = int(lengths.max())
+    pt, n_pages = synth.page_tables(lengths, page, g)
+    pool0 = dev(synth.random_bits16(g, (L, 2, n_pages, page, H * d)))
+    sc0 = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc0[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    sc0 = dev(sc0)
+    pos0 = dev(np.tile(np.arange(ld_s, dtype=np.int32), (B, 1)))
+    cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_band_a=na,
+                        n_band_b=nb, budget=K)
+    hid = dev(synth.f32_to_bf16_bits(
+        g.standard_normal((na + nb, B, C, D)).astype(np.float32)))
+    hidden = [hid[l] for l in range(na + nb)]
+    st_in = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
+    E.epikv_state_init(cfg, st_in)
+    torch.cuda.synchronize()
+    sec = E.state_sections(cfg, st_in)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32)).cuda()
+    st_out = torch.zeros_like(st_in)
+    st_tok = torch.zeros_like(st_in)
+    pool, scores, pos = pool0.clone(), sc0.clone(), pos0.clone()
+    tok_scores = torch.zeros_like(scores)
+    keep = torch.zeros((B, K), dtype=torch.int32, device="cuda")
+    n_keep = torch.zeros(B, dtype=torch.int32, device="cuda")
+    status = torch.zeros(B, dtype=torch.int32, device="cuda")
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    n_cached = dev(lengths.astype(np.int32))
+    io = E.make_step_io(
+        C, hidden, D, C * D, n_cached,
+        torch.zeros(B, dtype=torch.int32, device="cuda"),
+        E.pool_of(pool.view(L, 2, n_pages, page, H, d)), dev(pt), pt.shape[1],
+        E.Pool(), None, 0, scores, ld_s, st_in, st_out, keep, n_keep, status,
+        ws, ws_n, src_pos=pos, dst_pos=pos, in_place=True)
+
+    def work():
+        E.epikv_evict_step(cfg, io)
+        E.epikv_score_tokens(cfg, C, hidden, D, C * D, n_cached, st_in,
+                             st_tok, tok_scores, ld_s)
+
+    outs = (pool, scores, pos, keep, n_keep, status, st_out, st_tok,
+            tok_scores)
+
+    def reset():
+        for t in outs:
+            t.view(torch.uint8).fill_(0x5B)
+        pool.copy_(pool0)
+        scores.copy_(sc0)
+        pos.copy_(pos0)
+
+    def snapshot():
+        torch.cuda.synchronize()
+        return [host(t).copy() for t in outs]
+
+    reset()
+    work()
+    eager = snapshot()
+    assert np.all(eager[5] == 0)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        reset()
+        work()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        work()
+    junk = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        reset()
+        graph.replay()
+        got = snapshot()
+        for a, b in zip(got, eager):
+            assert a.tobytes() == b.tobytes(), rep
+        junk = junk * 1.0001 + 1.0
+        torch.cuda.synchronize()
