@@ -43,7 +43,8 @@ class Setup:
 def workload_kind(w: synth.Workload) -> str:
     """hs: a batch evicting after a chunk of new tokens; lagkv: the same
     with the Lag-KV signal; prefill: one trace scored in one shot; replay:
-    the single-sequence replays, which are parity tests only."""
+    one sequence at the steady state of a decode loop (timed hot and after
+    a cache scrub)."""
     if w.signal == "lagkv":
         return "lagkv"
     if w.chunk == w.n_max:
@@ -743,10 +744,8 @@ def main():
         sys.exit(1)
     w = synth.workload(args.workload)
     kind = workload_kind(w)
-    if kind == "replay" or ((args.online or args.inplace) and kind != "hs"):
-        print(f"workload {w.name} is a parity-test replay, not a bench line"
-              if kind == "replay" else
-              "--online and --inplace run on the hidden-state batch only",
+    if (args.online or args.inplace) and kind != "hs":
+        print("--online and --inplace run on the hidden-state batch only",
               file=sys.stderr)
         sys.exit(2)
     log(f"[bench] workload {w.name}: B={w.B} K={w.budget} C={w.chunk}")
@@ -758,8 +757,8 @@ def main():
             "unit": "us", "n_gpus": 1, "data": "synthetic",
             "results": rows}), flush=True)
         return
-    S = {"hs": setup_hs, "lagkv": setup_lag, "prefill": setup_prefill}[kind](
-        w, E)
+    S = {"hs": setup_hs, "replay": setup_hs, "lagkv": setup_lag,
+         "prefill": setup_prefill}[kind](w, E)
 
     # correctness guard: one step, every sequence must be OK with K kept
     E.epikv_evict_step(S.cfg, S.io)
@@ -790,6 +789,22 @@ def main():
         wall = time.perf_counter() - t0
         ms_step = wall / args.steps * 1e3
         log(f"[bench] evict_step: {ms_step:.3f} ms/step")
+    scrubbed_ms = None
+    if kind == "replay" and not args.stages_only:
+        # the same step with the caches flushed first: a 512 MiB write
+        # between steps, the step alone between two events
+        scrub = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+              for _ in range(args.steps)]
+        for i in range(args.steps):
+            scrub.fill_(float(i))
+            ev[i][0].record()
+            E.epikv_evict_step(S.cfg, S.io)
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        scrubbed_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        log(f"[bench] evict_step after a cache scrub: {scrubbed_ms:.4f} ms")
+        del scrub
     # per-stage durations with events on the launch stream
     n_ev = args.steps
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)]
@@ -834,6 +849,10 @@ def main():
                  f"normalised by the previous chunk's range, {w.n_layers} "
                  f"layers x {w.n_kv_heads} KV heads x {w.head_dim} bf16 "
                  f"paged, trailing mean w={w.window}",
+        "replay": f"{w.name}: one sequence at its steady state, "
+                  f"N={w.n_max} -> K={w.budget} after a {w.chunk}-token "
+                  f"chunk, {w.n_layers} layers x {w.n_kv_heads} KV heads x "
+                  f"{w.head_dim} bf16 paged, HS bands 7-13/18-25",
         "prefill": f"{w.name}: one {w.chunk}-token prefill scored in one "
                    f"shot (HS bands 7-13/18-25, z-score w={w.window}) and "
                    f"evicted to K={w.budget}, {w.n_layers} layers x "
@@ -861,6 +880,8 @@ def main():
             "n_cached": [int(x) for x in S.lengths],
             "algorithmic_bytes": ab,
             "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+            **({"ms_per_step_cache_scrubbed": round(scrubbed_ms, 4)}
+               if scrubbed_ms is not None else {}),
         },
         "roofline": {
             "kernel": dom_name,
@@ -876,7 +897,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample ...")
-        result["cpu_baseline"] = {"hs": cpu_baseline, "lagkv": cpu_baseline_lag,
+        result["cpu_baseline"] = {"hs": cpu_baseline, "replay": cpu_baseline,
+                                  "lagkv": cpu_baseline_lag,
                                   "prefill": cpu_baseline_prefill}[kind](w, S)
     print(json.dumps(result), flush=True)
 
