@@ -584,3 +584,25 @@ def test_first_hole():
     for _ in range(50):
         keep = O.select_keep(g.standard_normal(300), 40, 100, 25)
         assert O.first_hole(keep) >= 40
+
+
+# ---------------------------------------------------------------------------
+# The workloads' KV shape against the paper's capacity figures (Sec. 4.4,
+# App. I): 224 concurrent 32,768-token requests at a 2048-token budget
+# against 14 without eviction, projected for an 80 GB GPU from the per-token
+# cache size.
+# ---------------------------------------------------------------------------
+def test_kv_bytes_per_token_matches_capacity_figures():
+    w = synth.workload("ragged_batch32")
+    b = w.kv_bytes_per_token
+    assert b == 2 * 32 * 8 * 128 * 2 == 128 * 1024
+    # usable cache memory M implied by each figure: floor(M / bytes) = count
+    lo1, hi1 = 14 * 32768 * b, 15 * 32768 * b
+    lo2, hi2 = 224 * 2048 * b, 225 * 2048 * b
+    lo, hi = max(lo1, lo2), min(hi1, hi2)
+    assert lo < hi                           # both figures agree
+    # ... on about 60 GB: an 80 GB GPU less the ~16 GB of bf16 weights of an
+    # 8B-parameter model and some headroom
+    assert 55e9 < lo and hi < 64e9
+    # half the per-token size (4 KV heads) would leave only ~30 GB of cache
+    assert 224 * 2048 * (b // 2) < 31e9
