@@ -320,15 +320,18 @@ KV_SIGNALS = {  # name: (use keys, use values, lag-normalised)
     "kv_val": (False, True, False), "lagkv_key": (True, False, True)}
 
 
+@pytest.mark.parametrize("C", [64, 37, 200, 1])
 @pytest.mark.parametrize("signal", list(KV_SIGNALS))
-def test_kv_signals_match_oracle(E, signal):
+def test_kv_signals_match_oracle(E, signal, C):
+    """Chunk lengths that split a plane's rows between several workgroups
+    evenly (64), unevenly (37, 200) and not at all (1)."""
     import torch
-    print(f"kv signal {signal}", flush=True)
+    print(f"kv signal {signal} C={C}", flush=True)
     use_k, use_v, lag = KV_SIGNALS[signal]
     sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
               "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
     g = synth.rng(500)
-    L, H, d, page, B, C, w = 4, 8, 128, 16, 2, 64, 64
+    L, H, d, page, B, w = 4, 8, 128, 16, 2, 64
     n_chunks = 3
     T = C * n_chunks
     Ns = np.array([T, T + 16])       # seq 1 has 16 older tokens first
