@@ -319,3 +319,69 @@ def test_inplace_full_size_matches_out_of_place(E):
         assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, tail[b]),
                               tail_before[b]), b
     print(f"  rows moved: {moved} of {w.B * K}")
+
+
+def test_inplace_step_lagkv_matches_out_of_place(E):
+    """The Lag-KV step reads the chunk's K/V rows from the pool it then
+    rebuilds: in place it must give the scores, selection and rows of the
+    out-of-place step on the same inputs."""
+    import torch
+    print("in-place Lag-KV step", flush=True)
+    g = synth.rng(79)
+    B, C, K, page, L, H, d = 3, 64, 96, 16, 4, 8, 128
+    lengths = np.array([400, 150, 80])
+    ld_s = int(lengths.max())
+    pt, used = synth.page_tables(lengths, page, g)
+    dpt, n_dst = synth.contiguous_page_tables(np.full(B, K), page)
+    pool = synth.kv_rows(g, (L, 2, used, page, H, d)).reshape(
+        L, 2, used, page, H * d)
+    sc = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    cfg = E.default_cfg(batch=B, n_layers=L, signal=E.SIGNAL_LAGKV,
+                        smoothing=E.SMOOTH_MEAN, budget=K)
+    st0 = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
+    E.epikv_state_init(cfg, st0)
+    ws_n = E.workspace_bytes(cfg, C)
+
+    def run(in_place):
+        src = dev(pool)
+        dst = torch.zeros((L, 2, n_dst, page, H * d), dtype=torch.int16,
+                          device="cuda")
+        scores = dev(sc)
+        dsc = torch.zeros_like(scores)
+        keep = torch.zeros((B, K), dtype=torch.int32, device="cuda")
+        nk = torch.zeros(B, dtype=torch.int32, device="cuda")
+        status = torch.zeros(B, dtype=torch.int32, device="cuda")
+        st_out = torch.zeros_like(st0)
+        ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+        io = E.make_step_io(
+            C, None, 0, 0, dev(lengths.astype(np.int32)),
+            torch.zeros(B, dtype=torch.int32, device="cuda"),
+            E.pool_of(src.view(L, 2, used, page, H, d)), dev(pt), pt.shape[1],
+            E.Pool() if in_place else E.pool_of(
+                dst.view(L, 2, n_dst, page, H, d)),
+            None if in_place else dev(dpt), 0 if in_place else dpt.shape[1],
+            scores, ld_s, st0, st_out, keep, nk, status, ws, ws_n,
+            dst_scores=None if in_place else dsc, in_place=in_place)
+        E.epikv_evict_step(cfg, io)
+        torch.cuda.synchronize()
+        return (host(src), host(dst), host(scores), host(dsc), host(keep),
+                host(nk), host(status), host(st_out))
+
+    src_o, dst_o, sc_o, dsc_o, keep_o, nk_o, stat_o, st_o = run(False)
+    src_i, _, sc_i, _, keep_i, nk_i, stat_i, st_i = run(True)
+    assert np.all(stat_o == 0) and np.array_equal(stat_i, stat_o)
+    assert np.array_equal(nk_i, nk_o) and np.array_equal(keep_i, keep_o)
+    assert st_i.tobytes() == st_o.tobytes()
+    for b in range(B):
+        n = int(nk_o[b])
+        # scores: the out-of-place copy, or the sequence's own row if N <= K
+        ref = dsc_o[b, :n] if lengths[b] > K else sc_o[b, :n]
+        assert sc_i[b, :n].tobytes() == ref.tobytes(), b
+        got = gather_logical(src_i, pt[b], n)
+        if lengths[b] > K:
+            exp = gather_logical(dst_o, dpt[b], n)
+        else:
+            exp = gather_logical(pool, pt[b], n)
+        assert got.tobytes() == exp.tobytes(), b
