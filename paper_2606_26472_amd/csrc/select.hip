@@ -20,13 +20,15 @@
 // positions [t*KPT, (t+1)*KPT) in registers for all four sweeps, so step 2
 // needs two workgroup-wide scans in total.  Longer sequences re-read the
 // scores from global memory (L2) in each sweep and produce the output in
-// tiles of 1024 positions.
+// tiles of 8192 positions staged through LDS (two scans per tile).
 #include "epikv_internal.h"
 
 namespace epikv {
 namespace {
 
 constexpr int kWaves = kSelectThreads / 64;
+constexpr int kOutPer = 8;                         // long rows: positions per thread per tile
+constexpr int kOutTile = kOutPer * kSelectThreads;  // positions per output tile
 
 __device__ __forceinline__ uint32_t rank_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -103,6 +105,8 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
 template <int KPT>
 __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
   __shared__ uint32_t hist[2048];
+  // staging tile of the long-row output phase (unused by the register path)
+  __shared__ uint32_t out_tile[KPT > 0 ? 1 : kOutTile + kOutTile / kOutPer];
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t sel_digit, sel_above;
   const int tid = threadIdx.x;
@@ -168,9 +172,20 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
           atomicAdd(&hist[(keys[k] >> shift) & dmask], 1u);
       }
     } else {
-      for (int i = lo + tid; i < hi; i += kSelectThreads) {
-        const uint32_t key = rank_key(s[i]);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
+      // kOutPer scores per thread are loaded before any is counted
+      for (int i0 = lo + tid; i0 < hi; i0 += kOutPer * kSelectThreads) {
+        float v[kOutPer];
+#pragma unroll
+        for (int u = 0; u < kOutPer; ++u) {
+          const int i = i0 + u * kSelectThreads;
+          v[u] = i < hi ? s[i] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kOutPer; ++u) {
+          const uint32_t key = rank_key(v[u]);
+          if (i0 + u * kSelectThreads < hi && (key & mask) == prefix)
+            atomicAdd(&hist[(key >> shift) & dmask], 1u);
+        }
       }
     }
     __syncthreads();
@@ -242,25 +257,69 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a) {
       }
     }
   } else {
+    // Tiles of kOutTile positions: read coalesced into LDS (one pad word
+    // after every kOutPer, so the strided reads below hit distinct banks),
+    // then thread t takes the kOutPer contiguous positions
+    // [t*kOutPer, (t+1)*kOutPer) of the tile, so that two workgroup scans
+    // per tile rank the keys equal to T and place the kept positions in
+    // order.
+    float* tile_s = reinterpret_cast<float*>(out_tile);
     uint32_t eq_seen = 0u;
-    const int tiles = (N + kSelectThreads - 1) / kSelectThreads;
-#pragma unroll 1
-    for (int t = 0; t < tiles; ++t) {
-      const int i = t * kSelectThreads + tid;
-      const bool valid = i < N;
-      const bool prot = valid && (i < lo || i >= hi);
-      const bool elig = valid && !prot;
-      const uint32_t key = elig ? rank_key(s[i]) : 0u;
-      const bool gt = elig && key > T;
-      const bool eq = elig && key == T;
+    float nxt[kOutPer];  // the next tile's scores, loaded while this one is ranked
+#pragma unroll
+    for (int u = 0; u < kOutPer; ++u) {
+      const int k = u * kSelectThreads + tid;
+      nxt[u] = k < N ? s[k] : 0.f;
+    }
+    for (int t0 = 0; t0 < N; t0 += kOutTile) {
+#pragma unroll
+      for (int u = 0; u < kOutPer; ++u) {
+        const int k = u * kSelectThreads + tid;
+        tile_s[k + k / kOutPer] = nxt[u];
+        const int kn = t0 + kOutTile + k;
+        nxt[u] = kn < N ? s[kn] : 0.f;
+      }
+      __syncthreads();
+      const int q0 = tid * kOutPer;
+      uint32_t key[kOutPer];
+      uint32_t n_eq = 0u;
+#pragma unroll
+      for (int u = 0; u < kOutPer; ++u) {
+        const int i = t0 + q0 + u;
+        key[u] = rank_key(tile_s[q0 + tid + u]);  // padded: no bank conflicts
+        n_eq += (i >= lo && i < hi && key[u] == T) ? 1u : 0u;
+      }
       uint32_t eq_tot;
-      const uint32_t eq_rank = eq_seen + block_flag_rank(eq, wsum, &eq_tot);
-      const bool keep = prot || gt || (eq && eq_rank < need);
+      uint32_t eq_rank = eq_seen + block_exclusive_scan(n_eq, wsum, &eq_tot);
+      uint32_t keep_bits = 0u, n_keep_t = 0u;
+#pragma unroll
+      for (int u = 0; u < kOutPer; ++u) {
+        const int i = t0 + q0 + u;
+        if (i < N) {
+          const bool elig = i >= lo && i < hi;
+          bool keep = !elig || key[u] > T;
+          if (elig && key[u] == T) {
+            keep = eq_rank < need;
+            ++eq_rank;
+          }
+          if (keep) {
+            keep_bits |= 1u << u;
+            ++n_keep_t;
+          }
+        }
+      }
       uint32_t keep_tot;
-      const uint32_t slot = written + block_flag_rank(keep, wsum, &keep_tot);
-      if (keep && slot < (uint32_t)K) out[slot] = i;
+      uint32_t slot = written + block_exclusive_scan(n_keep_t, wsum, &keep_tot);
+#pragma unroll
+      for (int u = 0; u < kOutPer; ++u) {
+        if ((keep_bits >> u) & 1u) {
+          if (slot < (uint32_t)K) out[slot] = t0 + q0 + u;
+          ++slot;
+        }
+      }
       eq_seen += eq_tot;
       written += keep_tot;
+      __syncthreads();  // the tile buffer is refilled next
     }
   }
   if (tid == 0) {
