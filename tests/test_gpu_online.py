@@ -152,3 +152,30 @@ def test_score_tokens_equals_two_calls(E, mode, D):
                           state0=torch.from_numpy(st40).cuda())
         assert a[0].tobytes() == f[0].tobytes()
         assert a[1].tobytes() == f[1].tobytes()
+
+
+def test_state_checkpoint_and_resume(E):
+    """Checkpoint = a copy of the state buffer to the host.  Scoring a stream
+    in two halves, with the state saved after the first and restored into a
+    fresh device buffer, gives the scores and final state of the
+    uninterrupted run bit for bit."""
+    import torch
+    print("state checkpoint / resume", flush=True)
+    g = synth.rng(904)
+    B, T, D = 2, 200, 1024
+    w = synth.workload("drift_replay", B=B, hidden=D)
+    na, nb = len(w.band_a), len(w.band_b)
+    hid = np.stack([np.stack([synth.hidden_rows(
+        synth.amplitudes(w, g, 0, T)[l], D, g) for b in range(B)])
+        for l in range(w.n_band)])
+    cfg = E.default_cfg(batch=B, hidden=D, n_band_a=na, n_band_b=nb)
+    chunks = [16] * 12 + [8]
+    full_s, full_st = _score_stream(E, cfg, hid, chunks)
+    split = 7 * 16
+    s1, st1 = _score_stream(E, cfg, hid[:, :, :split], [16] * 7)
+    saved = np.array(st1, copy=True)              # the checkpoint (host bytes)
+    s2, st2 = _score_stream(E, cfg, hid[:, :, split:], [16] * 5 + [8],
+                            state0=torch.from_numpy(saved).cuda())
+    assert st2.tobytes() == full_st.tobytes()
+    assert s1.tobytes() == full_s[:, :split].tobytes()
+    assert s2.tobytes() == full_s[:, split:].tobytes()
