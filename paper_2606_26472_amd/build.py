@@ -1,6 +1,15 @@
 """Build libepikv.so (gfx950) in-tree with hipcc.
 
     python -m paper_2606_26472_amd.build
+    python -m paper_2606_26472_amd.build --host-asan   # _build/asan/libepikv.so
+
+The second form instruments the host code (argument validation, layouts,
+launch set-up) with AddressSanitizer; the device code is built as usual.  It
+is meant for the C-ABI validation tests on a machine without a GPU:
+
+    EPIKV_LIB=_build/asan/libepikv.so ASAN_OPTIONS=detect_leaks=0 \
+    LD_PRELOAD=$(ls /opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so) \
+    python -m pytest tests/test_abi.py -k "not only_the_c_abi"
 """
 from __future__ import annotations
 
@@ -46,14 +55,21 @@ def _run(cmd):
     return r
 
 
-def build(verbose: bool = False) -> str:
+ASAN_HOST = ["-Xarch_host", "-fsanitize=address",
+             "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build(verbose: bool = False, host_asan: bool = False) -> str:
     """Compile every source and link libepikv.so; returns its path."""
     cc = hipcc()
-    os.makedirs(BUILD, exist_ok=True)
+    out_dir = os.path.join(BUILD, "asan") if host_asan else BUILD
+    lib = os.path.join(out_dir, "libepikv.so") if host_asan else LIB
+    flags = CXXFLAGS + (ASAN_HOST if host_asan else [])
+    os.makedirs(out_dir, exist_ok=True)
 
     def compile_one(src):
-        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        cmd = [cc, *CXXFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
+        cmd = [cc, *flags, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         _run(cmd)
@@ -61,15 +77,16 @@ def build(verbose: bool = False) -> str:
 
     with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
+    # (an instrumented library takes its sanitizer runtime from LD_PRELOAD)
     cmd = [cc, "-shared", f"--offload-arch={ARCH}", "-fvisibility=hidden",
            "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     _run(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, host_asan="--host-asan" in sys.argv))

@@ -11,7 +11,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libepikv.so")
+# EPIKV_LIB selects another build of the same library (e.g. the host-ASan
+# one); a missing file is an error like a missing default build.
+LIB_PATH = os.environ.get("EPIKV_LIB") or os.path.join(_HERE, "libepikv.so")
 
 # status codes (include/epikv.h)
 EPIKV_OK = 0
