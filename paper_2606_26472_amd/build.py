@@ -27,7 +27,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libepikv.so")
 
 SOURCES = ["epikv_api.hip", "score_hs.hip", "score_lagkv.hip", "zscore.hip",
-           "select.hip", "compact.hip", "compact_inplace.hip", "score_tokens.hip"]
+           "select.hip", "compact.hip", "compact_inplace.hip", "score_tokens.hip",
+           "score_select.hip"]
 
 ARCH = "gfx950"
 CXXFLAGS = [

@@ -727,17 +727,34 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
 
   float* sig = (float*)ws;
   float* partial = (float*)(ws + sig_bytes(cfg, io->chunk));
-  st = run_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
-                 io->ld_src_pt, io->n_cached, io->state_in, io->state_out, sig, partial, stream);
-  if (st) return st;
-  st = launched(launch_zscore(zscore_args(cfg, io->chunk, sig, io->n_cached, io->state_in,
-                                          io->state_out, io->scores, io->ld_s, nullptr),
-                              stream));
-  if (st) return st;
-  st = launched(launch_select(select_args(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix,
-                                          io->keep_idx, io->n_keep, io->seq_status, io->chunk),
-                              stream));
-  if (st) return st;
+  const SelectArgs sel = select_args(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix,
+                                     io->keep_idx, io->n_keep, io->seq_status, io->chunk);
+  const ZscoreArgs zs = zscore_args(cfg, io->chunk, sig, io->n_cached, io->state_in, io->state_out,
+                                    io->scores, io->ld_s, nullptr);
+  bool fused = false;
+  if (cfg->signal == EPIKV_SIGNAL_HS) {
+    const ScoreHsArgs hs =
+        hs_args(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, io->state_in, io->state_out, sig);
+    if (select_score_fusable(sel, hs)) {
+      // The chunk lies inside the recency window: selection needs only the
+      // older, frozen scores, so it runs beside the scoring, then the
+      // chunk's scores are smoothed and written.
+      st = launched(launch_select_score(sel, hs, stream));
+      if (st) return st;
+      st = launched(launch_zscore(zs, stream));
+      if (st) return st;
+      fused = true;
+    }
+  }
+  if (!fused) {
+    st = run_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
+                   io->ld_src_pt, io->n_cached, io->state_in, io->state_out, sig, partial, stream);
+    if (st) return st;
+    st = launched(launch_zscore(zs, stream));
+    if (st) return st;
+    st = launched(launch_select(sel, stream));
+    if (st) return st;
+  }
   if (io->in_place)
     return launched(launch_compact_inplace(
         inplace_args(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep, io->scores,

@@ -248,6 +248,10 @@ hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r,
                               hipStream_t s);
 hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+// Selection and hidden-state scoring in one launch; valid only when
+// select_score_fusable (the chunk lies inside the recency window).
+bool select_score_fusable(const SelectArgs& sel, const ScoreHsArgs& sc);
+hipError_t launch_select_score(const SelectArgs& sel, const ScoreHsArgs& sc, hipStream_t s);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s);
 hipError_t launch_fill(const FillArgs& a, hipStream_t s);

@@ -319,3 +319,87 @@ def test_full_size_batched_step_sampled(E):
         assert np.array_equal(src_rows, dst_rows), b
         assert np.array_equal(host(S.dst_scores)[b, :K], gs[b, ref])
         assert np.array_equal(host(S.dst_pos)[b, :K], ref.astype(np.int32))
+
+
+@pytest.mark.parametrize("D,C,K", [(4096, 64, 256), (1000, 32, 512),
+                                   (4096, 100, 256)])
+def test_step_equals_its_stages(E, D, C, K):
+    """epikv_evict_step against its four stages called one by one on the
+    same inputs, bit for bit.  With C <= R (the first two cases) the step
+    selects and scores in one launch; with C > R (the third) it runs the
+    stages in order."""
+    import torch
+    print(f"step vs stages D={D} C={C} K={K}", flush=True)
+    g = synth.rng(950 + C)
+    B, L, H, d, page, na, nb = 4, 2, 8, 128, 16, 3, 2
+    nband = na + nb
+    lengths = np.array([900, 300, 600, 130])
+    ld_s = int(lengths.max())
+    cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_band_a=na,
+                        n_band_b=nb, budget=K)
+    R = O.default_recent(K)
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    pool = dev(synth.random_bits16(g, (L, 2, n_src, page, H * d)))
+    hid = dev(synth.f32_to_bf16_bits(
+        (g.standard_normal((nband, B, C, D)) * 2).astype(np.float32)))
+    hidden = [hid[l] for l in range(nband)]
+    sc = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    st_in = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
+    E.epikv_state_init(cfg, st_in)
+    torch.cuda.synchronize()
+    sec = E.state_sections(cfg, st_in)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32)).cuda()
+    sec["ring"][:] = torch.from_numpy((20.0 + g.standard_normal(
+        tuple(sec["ring"].shape))).astype(np.float32)).cuda()
+    sec["h_prev"][:] = torch.from_numpy(synth.f32_to_bf16_bits(
+        g.standard_normal(tuple(sec["h_prev"].shape)).astype(np.float32))
+        .view(np.int16)).cuda()
+    n_cached = dev(lengths.astype(np.int32))
+    n_prefix = dev(np.array([10, 0, 3, 0], np.int32))
+    pos = dev(np.tile(np.arange(ld_s, dtype=np.int32), (B, 1)))
+
+    def outputs():
+        return dict(
+            dst=torch.zeros((L, 2, n_dst, page, H * d), dtype=torch.int16,
+                            device="cuda"),
+            scores=dev(sc), dsc=torch.zeros((B, ld_s), device="cuda"),
+            dpos=torch.zeros((B, ld_s), dtype=torch.int32, device="cuda"),
+            keep=torch.full((B, K), -5, dtype=torch.int32, device="cuda"),
+            nk=torch.zeros(B, dtype=torch.int32, device="cuda"),
+            status=torch.zeros(B, dtype=torch.int32, device="cuda"),
+            st_out=torch.zeros_like(st_in))
+
+    src = E.pool_of(pool.view(L, 2, n_src, page, H, d))
+    spt, dpt = dev(src_pt), dev(dst_pt)
+    a = outputs()
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    io = E.make_step_io(
+        C, hidden, D, C * D, n_cached, n_prefix, src, spt, src_pt.shape[1],
+        E.pool_of(a["dst"].view(L, 2, n_dst, page, H, d)), dpt,
+        dst_pt.shape[1], a["scores"], ld_s, st_in, a["st_out"], a["keep"],
+        a["nk"], a["status"], ws, ws_n, dst_scores=a["dsc"], src_pos=pos,
+        dst_pos=a["dpos"])
+    E.epikv_evict_step(cfg, io)
+    s = outputs()
+    sig = torch.zeros((nband, B, C), device="cuda")
+    E.epikv_score(cfg, C, hidden, D, C * D, state_in=st_in,
+                  state_out=s["st_out"], sig=sig)
+    E.epikv_zscore(cfg, C, sig, n_cached, st_in, s["st_out"], s["scores"],
+                   ld_s)
+    E.epikv_select(cfg, s["scores"], ld_s, n_cached, n_prefix, s["keep"],
+                   s["nk"], s["status"])
+    cws_n = E.compact_workspace_bytes(cfg)
+    cws = torch.zeros(cws_n, dtype=torch.uint8, device="cuda")
+    E.epikv_compact(cfg, src, spt, src_pt.shape[1],
+                    E.pool_of(s["dst"].view(L, 2, n_dst, page, H, d)), dpt,
+                    dst_pt.shape[1], s["keep"], s["nk"], s["scores"],
+                    s["dsc"], pos, s["dpos"], ld_s, s["status"], cws, cws_n)
+    torch.cuda.synchronize()
+    assert (C <= R) == (C != 100)
+    for k in a:
+        assert host(a[k]).tobytes() == host(s[k]).tobytes(), k
+    assert np.all(host(a["status"]) == 0)
