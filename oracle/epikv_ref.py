@@ -50,6 +50,12 @@ READINGS = {
     "R18": "In-place rebuild (the move-minimising form): the retained rows "
            "are packed to the front of the sequence's own pages in order; "
            "slots past the retained count keep whatever they held.",
+    "R19": "Page remapping in the in-place rebuild: a destination page "
+           "whose slots receive, in order, every row of one later source "
+           "page takes that page in the page table instead of a copy; the "
+           "pages this frees are handed, in ascending order, to the source "
+           "positions that gave theirs away (ascending), so the sequence "
+           "keeps the same set of pages.",
     "R17": "EMA smoothing (App. E, alpha = 0.9): y(t) = alpha * y(t-1) + "
            "(1 - alpha) * x(t), starting at the stream's first sample "
            "(y = x); tokens without a sample leave y unchanged and get 0.",
@@ -405,3 +411,63 @@ def compact_rows_inplace(rows, keep):
     out = rows.copy()
     out[:keep.size] = rows[keep]
     return out
+
+
+def remap_pairs(keep, page_size):
+    """Whole-page retention (R19): the destination pages m (of the full
+    pages of the rebuilt sequence) whose page_size slots receive, in order,
+    all rows of one source page p, with p > m.  Ascending list of (m, p).
+    A page with p == m is already in place (the leading run)."""
+    keep = np.asarray(keep, dtype=np.int64)
+    ps = int(page_size)
+    pairs = []
+    for m in range(keep.size // ps):
+        run = keep[m * ps:(m + 1) * ps]
+        p, r = divmod(int(run[0]), ps)
+        if r == 0 and p > m and np.array_equal(run, np.arange(p * ps, (p + 1) * ps)):
+            pairs.append((m, p))
+    return pairs
+
+
+def page_table_after_remap(pt_row, keep, page_size):
+    """The sequence's page-table row after an in-place rebuild with page
+    remapping (R19): pair destination m takes the page of its source p; the
+    pages of destinations that are not themselves sources are released and
+    go, k-th to k-th in ascending order, to the sources that are not
+    themselves destinations.  Every other entry is unchanged, so the row is
+    a permutation of the old one."""
+    pairs = remap_pairs(keep, page_size)
+    dests = {m for m, _ in pairs}
+    srcs = {p for _, p in pairs}
+    old = np.asarray(pt_row)
+    new = old.copy()
+    for m, p in pairs:
+        new[m] = old[p]
+    released = [m for m, _ in pairs if m not in srcs]
+    losing = [p for _, p in pairs if p not in dests]
+    assert len(released) == len(losing)
+    for m, p in zip(released, losing):
+        new[p] = old[m]
+    return new
+
+
+def compact_pages_remap(pool, pt_row, keep, page_size):
+    """In-place rebuild of one sequence with page remapping (App. H, R18,
+    R19).  pool: physical pages [n_pages][page_size][...]; pt_row: the
+    sequence's page table.  Returns (pool after, page-table row after).
+    Through the new row, slot j < len(keep) reads the row that position
+    keep[j] held through the old row.  Slots of a remapped destination page
+    are not written (its page already holds them); every other slot j <
+    len(keep) is written with its row; nothing else changes."""
+    ps = int(page_size)
+    keep = np.asarray(keep, dtype=np.int64)
+    dests = {m for m, _ in remap_pairs(keep, ps)}
+    new_pt = page_table_after_remap(pt_row, keep, ps)
+    pool = np.asarray(pool)
+    out = pool.copy()
+    for j, i in enumerate(keep):
+        d = j // ps
+        if d in dests:
+            continue
+        out[new_pt[d], j % ps] = pool[pt_row[i // ps], i % ps]
+    return out, new_pt

@@ -606,3 +606,162 @@ def test_kv_bytes_per_token_matches_capacity_figures():
     assert 55e9 < lo and hi < 64e9
     # half the per-token size (4 KV heads) would leave only ~30 GB of cache
     assert 224 * 2048 * (b // 2) < 31e9
+
+
+# ---------------------------------------------------------------------------
+# App. H, in place with page remapping (R19): a destination page that
+# receives one later source page whole, in order, takes that page instead of
+# a copy
+# ---------------------------------------------------------------------------
+def _paged_case(g, N, ps, extra=3):
+    """A sequence of N tokens in ceil(N/ps) scattered physical pages of a
+    pool that also holds pages nobody owns."""
+    n_pg = -(-N // ps)
+    n_phys = n_pg + extra
+    pt = g.permutation(n_phys)[:n_pg].astype(np.int64)
+    pool = synth.random_bits16(g, (n_phys, ps, 3))
+    return pool, pt
+
+
+def _walk_through_tables(pool, old_pt, new_pt, keep, ps, skip_pages):
+    """Independent check of the in-place walk: slots in ascending order, each
+    row read through the old table and written through the new one, in one
+    buffer, asserting that no row is read after it was overwritten."""
+    buf = pool.copy()
+    written = set()
+    for j, i in enumerate(keep):
+        d = j // ps
+        if d in skip_pages:
+            continue
+        src = (int(old_pt[i // ps]), int(i % ps))
+        dst = (int(new_pt[d]), j % ps)
+        assert src not in written or src == dst, "row overwritten before read"
+        buf[dst] = buf[src].copy()
+        written.add(dst)
+    return buf, written
+
+
+def test_remap_evicting_an_aligned_block_only_rotates_the_table():
+    # evicting e whole pages starting at page a moves every later page e
+    # places forward: the rebuild is a rotation of the table, no row copied
+    g = synth.rng(21)
+    for ps, n, a, e in [(4, 4, 1, 1), (4, 8, 2, 3), (16, 10, 0, 2),
+                        (1, 9, 3, 2), (3, 7, 6, 1)]:
+        N = n * ps
+        pool, pt = _paged_case(g, N, ps)
+        keep = np.array([i for i in range(N)
+                         if not a * ps <= i < (a + e) * ps])
+        new_pool, new_pt = O.compact_pages_remap(pool, pt, keep, ps)
+        expect = np.concatenate([pt[:a], pt[a + e:], pt[a:a + e]])
+        assert new_pt.tolist() == expect.tolist()
+        assert new_pool.tobytes() == pool.tobytes()       # nothing written
+        assert O.remap_pairs(keep, ps) == [(m, m + e) for m in range(a, n - e)]
+
+
+def test_remap_hand_example():
+    # 4-token pages, page table [10, 11, 12, 13]; positions 4..7 evicted:
+    # slots 4..7 take page 12 and slots 8..11 page 13, the page that held
+    # positions 4..7 (11) goes to the position page 13 left
+    pt = np.array([10, 11, 12, 13])
+    keep = np.array([0, 1, 2, 3, 8, 9, 10, 11, 12, 13, 14, 15])
+    assert O.remap_pairs(keep, 4) == [(1, 2), (2, 3)]
+    assert O.page_table_after_remap(pt, keep, 4).tolist() == [10, 12, 13, 11]
+    # one more token evicted inside page 3: page 1 still takes page 2 whole,
+    # slots 8..10 are copied from positions 12, 13, 15 into page 11
+    keep = np.array([0, 1, 2, 3, 8, 9, 10, 11, 12, 13, 15])
+    assert O.remap_pairs(keep, 4) == [(1, 2)]
+    assert O.page_table_after_remap(pt, keep, 4).tolist() == [10, 12, 11, 13]
+
+
+def test_remap_with_no_whole_page_equals_plain_inplace():
+    # a shift that is not a multiple of the page size leaves no whole page:
+    # the table is unchanged and the pool is the plain in-place rebuild
+    g = synth.rng(22)
+    ps, N = 4, 40
+    pool, pt = _paged_case(g, N, ps)
+    keep = np.array([i for i in range(N) if i not in (5, 17, 30)])
+    assert O.remap_pairs(keep, ps) == []
+    new_pool, new_pt = O.compact_pages_remap(pool, pt, keep, ps)
+    assert new_pt.tolist() == pt.tolist()
+    rows = pool[pt].reshape(N, 3)
+    moved = O.compact_rows_inplace(rows, keep)
+    assert new_pool[pt].reshape(N, 3).tobytes() == moved.tobytes()
+
+
+def test_remap_brute_force_small():
+    # every ascending retained set of up to 9 tokens, page sizes 1..4
+    g = synth.rng(23)
+    import itertools
+    n_cases = n_pairs = 0
+    for ps in (1, 2, 3, 4):
+        for N in range(0, 10):
+            pool, pt = _paged_case(g, N, ps)
+            for r in range(N + 1):
+                for keep in itertools.combinations(range(N), r):
+                    keep = np.array(keep, dtype=np.int64)
+                    new_pool, new_pt = O.compact_pages_remap(pool, pt, keep, ps)
+                    pairs = O.remap_pairs(keep, ps)
+                    n_cases += 1
+                    n_pairs += len(pairs)
+                    # the row is a permutation of the old one
+                    assert sorted(new_pt.tolist()) == sorted(pt.tolist())
+                    # logical content: slot j holds the row of keep[j]
+                    for j, i in enumerate(keep):
+                        got = new_pool[new_pt[j // ps], j % ps]
+                        assert got.tobytes() == pool[pt[i // ps], i % ps].tobytes()
+                    # walked in ascending slot order inside one buffer, no
+                    # row is overwritten before it is read, and the result is
+                    # the oracle's
+                    skip = {m for m, _ in pairs}
+                    buf, written = _walk_through_tables(pool, pt, new_pt, keep,
+                                                        ps, skip)
+                    assert buf.tobytes() == new_pool.tobytes()
+                    # only slots of the sequence's own pages are written, and
+                    # none of a remapped page; pages nobody owns are unchanged
+                    own = set(pt.tolist())
+                    assert all(p in own for p, _ in written)
+                    assert not any(new_pt[m] == p for p, _ in written
+                                   for m in skip)
+                    assert len(written) == len(keep) - ps * len(pairs)
+                    other = sorted(set(range(pool.shape[0])) - own)
+                    assert new_pool[other].tobytes() == pool[other].tobytes()
+    assert n_cases > 2000 and n_pairs > 500
+
+
+def test_remap_release_order_matters():
+    # handing the released pages over in descending order would overwrite a
+    # row before it is read: the ascending order of R19 is what makes the
+    # front-to-back walk safe
+    # (with fewer than two released pages the order cannot differ: search
+    # the 2-token-page cases for one with two)
+    ps = 2
+    g = synth.rng(24)
+    found = False
+    import itertools
+    for N in range(6, 13):
+        pool, pt = _paged_case(g, N, ps, extra=0)
+        for r in range(N + 1):
+            for keep in itertools.combinations(range(N), r):
+                keep = np.array(keep)
+                pairs = O.remap_pairs(keep, ps)
+                dests = {m for m, _ in pairs}
+                srcs = {p for _, p in pairs}
+                rel = [m for m, _ in pairs if m not in srcs]
+                lose = [p for _, p in pairs if p not in dests]
+                if len(rel) < 2:
+                    continue
+                wrong = pt.copy()
+                for m, p in pairs:
+                    wrong[m] = pt[p]
+                for m, p in zip(rel, reversed(lose)):
+                    wrong[p] = pt[m]
+                try:
+                    _walk_through_tables(pool, pt, wrong, keep, ps, dests)
+                except AssertionError:
+                    found = True
+                    break
+            if found:
+                break
+        if found:
+            break
+    assert found
