@@ -408,6 +408,22 @@ def first_holes(keep, n_keep):
     return np.array(out)
 
 
+def whole_pages(keep, n_keep, page):
+    """Destination pages that take a whole source page (page remapping):
+    full pages whose slots hold one later, aligned source page in order."""
+    total = 0
+    for b in range(keep.shape[0]):
+        n = int(n_keep[b]) // page * page
+        if n <= 0:
+            continue
+        runs = keep[b, :n].reshape(-1, page).astype(np.int64)
+        first = runs[:, 0]
+        ok = ((first % page == 0) & (first > np.arange(runs.shape[0]) * page)
+              & (runs[:, -1] - first == page - 1))
+        total += int(ok.sum())
+    return total
+
+
 def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
                         scores, dscores, ld_s, status, cws, reps):
     """Time epikv_compact and epikv_compact_inplace on the same kept sets.
@@ -425,12 +441,23 @@ def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
     ms_in = _time_calls(lambda: E.epikv_compact_inplace(
         cfg, src, src_pt, src_pt.shape[1], keep, n_keep, scores, None, ld_s,
         status, cws, cws.numel()), reps)
+    # page remapping rewrites the table: each call permutes a copy again,
+    # with the same pages remapped and the same rows moved every time
+    pt_copy = src_pt.clone()
+    ms_remap = _time_calls(lambda: E.epikv_compact_remap(
+        cfg, src, pt_copy, src_pt.shape[1], keep, n_keep, scores, None, ld_s,
+        status, cws, cws.numel()), reps)
+    pages = whole_pages(kh, nk, w.page_size)
+    moved_remap = moved - pages * w.page_size
     out_bytes = kept * (2 * row + 8)
     in_bytes = moved * (2 * row + 8)
     return {"rows_kept": kept, "rows_moved_in_place": moved,
+            "pages_remapped": pages, "rows_moved_remap": moved_remap,
             "ms_out_of_place": round(ms_out, 4), "ms_in_place": round(ms_in, 4),
+            "ms_remap": round(ms_remap, 4),
             "gbps_out_of_place": round(out_bytes / ms_out / 1e6, 1),
-            "gbps_in_place": round(in_bytes / ms_in / 1e6, 1)}
+            "gbps_in_place": round(in_bytes / ms_in / 1e6, 1),
+            "gbps_remap": round(moved_remap * (2 * row) / ms_remap / 1e6, 1)}
 
 
 def inplace_report(E, S, w, reps):
@@ -478,6 +505,23 @@ def inplace_report(E, S, w, reps):
                          f"-> K={K}, protected prefill P={P}")
         out.append(r)
         log(f"[inplace] {r}")
+    # 3. the best case of page remapping: the evicted tokens fill whole
+    # aligned pages (here the lowest scores are C/page whole pages)
+    for b in range(B):
+        pages = g.choice((K - C) // page, size=C // page, replace=False)
+        for a in pages:
+            sc[b, a * page:(a + 1) * page] -= 1000.0
+    scores.copy_(torch.from_numpy(sc))
+    n_prefix = torch.zeros((B,), dtype=torch.int32, device=dev)
+    E.epikv_select(S.cfg, scores, K + C, n_cached, n_prefix, S.keep_idx,
+                   S.n_keep, S.status)
+    r = compare_compactions(E, S.cfg, w, src, spt, dst, dpt, S.keep_idx,
+                            S.n_keep, scores, dscores, K + C, S.status,
+                            S.cws, reps)
+    r["workload"] = (f"steady-state decode eviction, evicted tokens in whole "
+                     f"pages: B={B}, N={K + C} -> K={K}")
+    out.append(r)
+    log(f"[inplace] {r}")
     return out
 
 

@@ -171,9 +171,11 @@ int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
  * of `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
 
-/* Device scratch of epikv_compact and epikv_compact_inplace: 16 bytes per
- * (sequence, kept slot), B*K*16 rounded up to 256, then 8 bytes per sequence
- * rounded up to 256.  0 for an invalid cfg. */
+/* Device scratch of epikv_compact, epikv_compact_inplace and
+ * epikv_compact_remap: 16 bytes per (sequence, kept slot), B*K*16 rounded up
+ * to 256, then 8 bytes per sequence rounded up to 256, then 16 bytes per
+ * (sequence, page of the budget), B*ceil(K/page_size)*16 rounded up to 256.
+ * 0 for an invalid cfg. */
 size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg);
 
 /* Reset a state buffer of epikv_state_bytes(cfg) bytes to the start of a
@@ -339,6 +341,35 @@ int epikv_compact_inplace(const epikv_cfg* cfg, const epikv_pool* pool,
                           float* scores, int32_t* pos, int64_t ld_s,
                           int32_t* seq_status, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * epikv_compact_remap -- epikv_compact_inplace with whole-page retention
+ * (the page-table form of the move-minimising rebuild of App. H).
+ *
+ * The result, read through the page table after the call, is the same as
+ * epikv_compact_inplace's: slot j < min(n_keep[b], K) holds the row position
+ * keep_idx[b][j] held before, for every layer, K and V.  But a full
+ * destination page m whose page_size slots receive, in order, every row of
+ * one source page p > m is not copied: page_table[b][m] takes that page.  The
+ * pages of such destinations that are not themselves such sources go, k-th
+ * to k-th in ascending position order, to the positions of the sources that
+ * are not themselves such destinations.  page_table[b] stays a permutation
+ * of its old entries (only positions below ceil((keep_idx[b][n_keep-1]+1) /
+ * page_size) change), so the sequence owns the same pages; rows are written
+ * only at slots >= the first hole that lie outside remapped pages.  Evicting
+ * whole aligned pages therefore moves no row at all.
+ *
+ * page_table (int32 [B][ld_pt]) is read and rewritten on the device; it must
+ * overlap neither keep_idx, n_keep nor the workspace (EPIKV_EALIAS).  Everything else -- arguments,
+ * checks, flagged sequences (left untouched, table included), the optional
+ * scores and pos, the workspace -- is as for epikv_compact_inplace.
+ */
+int epikv_compact_remap(const epikv_cfg* cfg, const epikv_pool* pool,
+                        int32_t* page_table, int64_t ld_pt,
+                        const int32_t* keep_idx, const int32_t* n_keep,
+                        float* scores, int32_t* pos, int64_t ld_s,
+                        int32_t* seq_status, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
 
 /* Arguments of one eviction step (host struct; pointers as above). */
 typedef struct epikv_step_io {

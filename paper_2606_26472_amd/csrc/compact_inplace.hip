@@ -43,6 +43,163 @@ __device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
   return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
+// Exclusive rank of this thread's flag among the workgroup's set flags (in
+// thread order), and the workgroup total.
+__device__ __forceinline__ int flag_rank(bool flag, int* wsum, int* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const uint64_t m = __ballot(flag);
+  if (lane == 0) wsum[wave] = __popcll(m);
+  __syncthreads();
+  int pre = 0, tot = 0;
+  for (int w = 0; w < kInplaceThreads / 64; ++w) {
+    const int x = wsum[w];
+    pre += (w < wave) ? x : 0;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + __popcll(m & ((1ull << lane) - 1ull));
+}
+
+// Index of `v` in the strictly ascending keep[0, n), or -1.
+__device__ __forceinline__ int find_kept(const int32_t* keep, int n, int64_t v) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (keep[mid] < v) lo = mid + 1; else hi = mid;
+  }
+  return (lo < n && keep[lo] == v) ? lo : -1;
+}
+
+// Whole-page retention.  A destination page m (a full page of the rebuilt
+// sequence) whose slots receive, in order, all rows of one source page p > m
+// is not copied: the table entry m takes p's page.  The pages of such
+// destinations that are not themselves such sources are released and go,
+// k-th to k-th in ascending order, to the sources that are not themselves
+// destinations, so the row stays a permutation of the sequence's pages.  A
+// released page (that of m) then only receives rows at slots of a later
+// page than m, after every slot that reads it in the front-to-back walk.
+//
+// Runs inside the check kernel once keep_idx is known to be valid: rewrites
+// the destination half of the offset records of the moved slots, drops the
+// records of remapped pages (their rows do not move) and then rewrites the
+// table.  Per sequence, in the
+// workspace, indexed by destination page:
+//   src[m]  p if m is remapped, else -1
+//   npg[m]  the page slot m*page_size.. writes to (remapped: the table value)
+//   give[m] the rank, then the page, handed to position src[m] when that
+//           position is not a destination itself, else -1
+// and by rank: rel[k] the k-th released page.
+__device__ void remap_pages(const InplaceArgs& a, int b, const int32_t* keep, const int32_t* pt,
+                            int nk, int hole, int64_t* rec) {
+  __shared__ int s_sum[kInplaceThreads / 64];
+  const int tid = threadIdx.x;
+  const int ps = a.page_size;
+  const int npd = nk / ps;                // full destination pages
+  const int ndp = (nk + ps - 1) / ps;     // destination pages
+  const int m0 = hole / ps;               // the leading run's pages stay
+  int32_t* src = a.remap_ws + (int64_t)b * 4 * a.n_pg;
+  int32_t* npg = src + a.n_pg;
+  int32_t* give = npg + a.n_pg;
+  int32_t* rel = give + a.n_pg;
+
+  for (int m = m0 + tid; m < ndp; m += kInplaceThreads) {
+    int p = -1;
+    if (m < npd) {
+      const int k0 = keep[m * ps];
+      const int k1 = keep[m * ps + ps - 1];
+      // keep is strictly ascending, so a span of ps - 1 means consecutive
+      if (k0 % ps == 0 && k0 > m * ps && k1 - k0 == ps - 1) p = k0 / ps;
+    }
+    src[m] = p;
+    npg[m] = pt[p >= 0 ? p : m];
+    give[m] = -1;
+  }
+  wait_vmem();
+  __syncthreads();
+
+  int n_rel = 0, n_give = 0;
+  for (int t0 = m0; t0 < npd; t0 += kInplaceThreads) {
+    const int m = t0 + tid;
+    const int p = m < npd ? src[m] : -1;
+    bool released = false, gives = false;
+    if (p >= 0) {
+      // m is itself a source if some remapped destination takes page m
+      const int j = find_kept(keep, nk, (int64_t)m * ps);
+      const bool is_src = j >= 0 && j % ps == 0 && j / ps >= m0 && j / ps < npd && src[j / ps] == m;
+      released = !is_src;
+      gives = !(p < npd && src[p] >= 0);
+    }
+    int tot_rel, tot_give;
+    const int r_rel = n_rel + flag_rank(released, s_sum, &tot_rel);
+    const int r_give = n_give + flag_rank(gives, s_sum, &tot_give);
+    if (released) rel[r_rel] = pt[m];
+    if (gives) give[m] = r_give;
+    n_rel += tot_rel;
+    n_give += tot_give;
+  }
+  // The two counts agree for every strictly ascending keep_idx; should they
+  // not, the sequence is rebuilt without remapping rather than with a page
+  // nobody handed over.
+  if (n_rel != n_give) return;
+  wait_vmem();
+  __syncthreads();
+
+  for (int m = m0 + tid; m < npd; m += kInplaceThreads) {
+    const int r = give[m];
+    if (r >= 0) {
+      const int page = rel[r];
+      give[m] = page;
+      const int p = src[m];
+      if (p < ndp) npg[p] = page;
+    }
+  }
+  wait_vmem();
+  __syncthreads();
+
+  // The records of the rows that still move, packed in ascending slot order
+  // from index `hole` on (the walk needs only their order), tile by tile:
+  // every record of a tile is read before any is written, and a row's
+  // packed index never exceeds its slot.
+  int n_mv = 0;
+  for (int j0 = hole; j0 < nk; j0 += kInplaceThreads) {
+    const int j = j0 + tid;
+    bool mv = false;
+    int64_t so = -1, dso = -1;
+    if (j < nk) {
+      const int d = j / ps;
+      mv = !(d < npd && src[d] >= 0);
+      if (mv) {
+        so = rec[2 * j];
+        dso = (int64_t)npg[d] * a.s_page + (int64_t)(j - d * ps) * a.row_bytes;
+      }
+    }
+    wait_vmem();
+    int tot;
+    const int k = hole + n_mv + flag_rank(mv, s_sum, &tot);
+    if (mv) {
+      rec[2 * k] = so;
+      rec[2 * k + 1] = dso;
+    }
+    n_mv += tot;
+  }
+  if (tid == 0) a.info[2 * b + 1] = hole + n_mv;
+  // every read of the old table is behind this barrier
+  wait_vmem();
+  __syncthreads();
+
+  int32_t* out = a.pt_out + (int64_t)b * a.ld_pt;
+  for (int m = m0 + tid; m < npd; m += kInplaceThreads) {
+    const int p = src[m];
+    if (p >= 0) {
+      out[m] = npg[m];
+      const int page = give[m];
+      if (page >= 0) out[p] = page;
+    }
+  }
+}
+
 __global__ __launch_bounds__(kInplaceThreads) void k_inplace_check(InplaceArgs a) {
   __shared__ int s_bad[kInplaceThreads / 64];
   __shared__ int s_hole[kInplaceThreads / 64];
@@ -108,6 +265,11 @@ __global__ __launch_bounds__(kInplaceThreads) void k_inplace_check(InplaceArgs a
   if (tid == 0) {
     info[0] = hole;
     info[1] = nk;
+  }
+  if (a.remap) {
+    remap_pages(a, b, keep, pt, nk, hole, rec);
+    wait_vmem();
+    __syncthreads();
   }
   if (!side) return;
   // Scores and positions follow their rows, in ascending tiles (the same

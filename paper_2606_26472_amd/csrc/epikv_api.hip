@@ -76,8 +76,13 @@ size_t compact_records_bytes(const epikv_cfg* c) {
   return align_up(16 * (size_t)c->batch * (size_t)c->budget);
 }
 
+int budget_pages(const epikv_cfg* c) {
+  return (int)(((int64_t)c->budget + c->page_size - 1) / c->page_size);
+}
+
 size_t compact_ws_bytes(const epikv_cfg* c) {
-  return compact_records_bytes(c) + align_up(8 * (size_t)c->batch);
+  return compact_records_bytes(c) + align_up(8 * (size_t)c->batch) +
+         align_up(16 * (size_t)c->batch * (size_t)budget_pages(c));
 }
 
 // Workgroups sharing the rows of one (plane, sequence) in the KV-vector
@@ -495,6 +500,10 @@ InplaceArgs inplace_args(const epikv_cfg* c, const epikv_pool* pool, const int32
   a.seq_status = seq_status;
   a.offsets = (int64_t*)ws;
   a.info = (int32_t*)((char*)ws + compact_records_bytes(c));
+  a.remap = 0;
+  a.pt_out = nullptr;
+  a.remap_ws = (int32_t*)((char*)ws + compact_records_bytes(c) + align_up(8 * (size_t)c->batch));
+  a.n_pg = budget_pages(c);
   a.B = c->batch;
   a.K = c->budget;
   a.page_size = c->page_size;
@@ -683,6 +692,26 @@ EPIKV_EXPORT int epikv_compact_inplace(const epikv_cfg* cfg, const epikv_pool* p
   return launched(launch_compact_inplace(inplace_args(cfg, pool, page_table, ld_pt, keep_idx, n_keep,
                                                       scores, pos, ld_s, seq_status, workspace),
                                          stream));
+}
+
+EPIKV_EXPORT int epikv_compact_remap(const epikv_cfg* cfg, const epikv_pool* pool,
+                                     int32_t* page_table, int64_t ld_pt, const int32_t* keep_idx,
+                                     const int32_t* n_keep, float* scores, int32_t* pos,
+                                     int64_t ld_s, int32_t* seq_status, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  int st = check_compact_inplace(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos, ld_s,
+                                 workspace, workspace_bytes);
+  if (st) return st;
+  const size_t pt_bytes = 4 * (size_t)cfg->batch * (size_t)ld_pt;
+  if (overlap(page_table, pt_bytes, keep_idx, 4 * (size_t)cfg->batch * (size_t)cfg->budget) ||
+      overlap(page_table, pt_bytes, n_keep, 4 * (size_t)cfg->batch) ||
+      overlap(page_table, pt_bytes, workspace, workspace_bytes))
+    return EPIKV_EALIAS;
+  InplaceArgs a = inplace_args(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos, ld_s,
+                               seq_status, workspace);
+  a.remap = 1;
+  a.pt_out = page_table;
+  return launched(launch_compact_inplace(a, stream));
 }
 
 EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io, hipStream_t stream) {

@@ -156,6 +156,13 @@ struct InplaceArgs {
   int32_t* seq_status;                     // optional
   int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
   int32_t* info;                           // workspace [B][2]: first hole, rows kept
+  // Page remapping (whole retained pages change places in the table instead
+  // of being copied): pt_out is the same table, written; remap_ws holds four
+  // int32 arrays of n_pg = ceil(K / page_size) entries per sequence.
+  int32_t remap;
+  int32_t* pt_out;
+  int32_t* remap_ws;                       // workspace [B][4][n_pg]
+  int32_t n_pg;
   int32_t B, K, page_size, row_bytes, n_lk;
   int32_t lanes_per_row;                   // 64, 16 or 4 lanes share one row of a plane
   int32_t n_slices;                        // ceil(row_bytes / 16 / lanes_per_row)

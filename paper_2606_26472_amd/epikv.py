@@ -45,7 +45,8 @@ EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_workspace_bytes", "epikv_compact_workspace_bytes",
             "epikv_state_init", "epikv_score", "epikv_score_tokens",
             "epikv_zscore", "epikv_select", "epikv_compact",
-            "epikv_compact_inplace", "epikv_evict_step")
+            "epikv_compact_inplace", "epikv_compact_remap",
+            "epikv_evict_step")
 
 
 class EpikvError(RuntimeError):
@@ -127,6 +128,8 @@ def lib() -> ctypes.CDLL:
                                          P, P, P, P, P, P, i64, P, P, sz, P]),
         "epikv_compact_inplace": (ctypes.c_int, [cfgp, poolp, P, i64, P, P,
                                                  P, P, i64, P, P, sz, P]),
+        "epikv_compact_remap": (ctypes.c_int, [cfgp, poolp, P, i64, P, P,
+                                               P, P, i64, P, P, sz, P]),
         "epikv_evict_step": (ctypes.c_int, [cfgp, ctypes.POINTER(StepIO), P]),
     }
     for name, (res, args) in sig.items():
@@ -283,6 +286,17 @@ def epikv_compact_inplace(cfg: Cfg, pool: Pool, page_table, ld_pt, keep_idx,
         _ptr(keep_idx), _ptr(n_keep), _ptr(scores), _ptr(pos), int(ld_s),
         _ptr(seq_status), _ptr(workspace), int(workspace_bytes_),
         _stream(stream)), "epikv_compact_inplace")
+
+
+def epikv_compact_remap(cfg: Cfg, pool: Pool, page_table, ld_pt, keep_idx,
+                        n_keep, scores=None, pos=None, ld_s=0,
+                        seq_status=None, workspace=None, workspace_bytes_=0,
+                        stream=None):
+    _check(lib().epikv_compact_remap(
+        ctypes.byref(cfg), ctypes.byref(pool), _ptr(page_table), int(ld_pt),
+        _ptr(keep_idx), _ptr(n_keep), _ptr(scores), _ptr(pos), int(ld_s),
+        _ptr(seq_status), _ptr(workspace), int(workspace_bytes_),
+        _stream(stream)), "epikv_compact_remap")
 
 
 def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,

@@ -96,7 +96,8 @@ def test_state_layout_sizes(E):
     assert E.workspace_bytes(c, 128) >= 4 * 15 * 32 * 128
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
     assert E.workspace_bytes(c, 0) == 0
-    assert E.compact_workspace_bytes(c) == 16 * 32 * 4096 + 256
+    # records, per-sequence info, four page arrays per sequence
+    assert E.compact_workspace_bytes(c) == 16 * 32 * 4096 + 256 + 16 * 32 * 256
     assert E.workspace_bytes(c, 128) >= E.compact_workspace_bytes(c) \
         + 4 * 15 * 32 * 128
 
@@ -296,7 +297,7 @@ def test_compact_inplace_validation(E):
     bad = E.Pool(None, 0, 0, 0, 0)
     W = 4 * A
     n = E.compact_workspace_bytes(c)
-    assert n == 16 * 2 * 256 + 256       # records, then per-sequence info
+    assert n == 16 * 2 * 256 + 256 + 512  # records, info, page arrays
     assert f(ctypes.byref(c), ctypes.byref(bad), A, 4, A, A, None, None, 0,
              None, W, n, None) == E.EPIKV_EINVAL_NULL
     assert f(ctypes.byref(c), ctypes.byref(pool), None, 4, A, A, None, None,
@@ -311,6 +312,29 @@ def test_compact_inplace_validation(E):
              None, W, n, None) == E.EPIKV_EINVAL_SHAPE      # scores, ld_s 0
     assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, A, A + 64, 100,
              None, W, n, None) == E.EPIKV_EALIAS            # scores on pos
+
+
+@host_only
+def test_compact_remap_validation(E):
+    L = E.lib()
+    c = E.default_cfg(batch=2, budget=256)
+    f = L.epikv_compact_remap
+    pool = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
+    W = 4 * A
+    n = E.compact_workspace_bytes(c)
+    assert f(ctypes.byref(c), ctypes.byref(pool), None, 4, A, A, None, None,
+             0, None, W, n, None) == E.EPIKV_EINVAL_NULL
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A, A, None, None, 0,
+             None, W, n - 1, None) == E.EPIKV_EWORKSPACE
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 0, A, A, None, None, 0,
+             None, W, n, None) == E.EPIKV_EINVAL_SHAPE      # ld_pt < 1
+    # the table is rewritten: it may overlap neither keep_idx nor workspace
+    assert f(ctypes.byref(c), ctypes.byref(pool), A, 4, A + 16, A, None,
+             None, 0, None, W, n, None) == E.EPIKV_EALIAS
+    assert f(ctypes.byref(c), ctypes.byref(pool), W + 256, 4, A, A, None,
+             None, 0, None, W, n, None) == E.EPIKV_EALIAS
+    assert f(ctypes.byref(c), ctypes.byref(pool), 2 * A, 4, A, 2 * A + 8,
+             None, None, 0, None, W, n, None) == E.EPIKV_EALIAS  # n_keep
 
 
 @host_only
