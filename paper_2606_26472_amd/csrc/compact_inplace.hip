@@ -13,9 +13,9 @@
 //          the scores and positions.  A sequence that fails the check is left
 //          untouched and flagged RANGE.
 //   move   one wavefront per (sequence, plane, column slice) walks the moved
-//          slots in ascending order, a tile of T rows at a time: it loads the
-//          tile's source rows, waits until every load has returned, then
-//          stores them.  A store to slot j can only overwrite a row that a
+//          slots in ascending order, a tile of T rows at a time (16 to 256,
+//          deeper when there are few walks): it loads the tile's source rows,
+//          waits until every load has returned, then stores them.  A store to slot j can only overwrite a row that a
 //          slot <= j reads; slots of this tile have read theirs, and slots of
 //          later tiles read rows past the end of this tile (their sources
 //          are >= their own slots).  So one wavefront per column slice moves
@@ -296,9 +296,10 @@ __global__ __launch_bounds__(kInplaceThreads) void k_inplace_check(InplaceArgs a
 
 template <int LPR, int NI>
 __global__ __launch_bounds__(kCompactThreads) void k_inplace_move(InplaceArgs a) {
-  constexpr int RPI = 64 / LPR;  // rows per load instruction
-  constexpr int T = RPI * NI;    // rows per tile
-  static_assert(T <= 64, "one record per lane");
+  constexpr int RPI = 64 / LPR;          // rows per load instruction
+  constexpr int T = RPI * NI;            // rows per tile
+  constexpr int RPL = (T + 63) / 64;     // records per lane
+  static_assert(T <= 64 || T % 64 == 0, "a tile fills whole record registers");
   const int lane = threadIdx.x & 63;
   const int64_t unit = (int64_t)blockIdx.x * kCompactWaves + (threadIdx.x >> 6);
   const int64_t per_seq = (int64_t)a.n_lk * a.n_slices;
@@ -315,11 +316,16 @@ __global__ __launch_bounds__(kCompactThreads) void k_inplace_move(InplaceArgs a)
   const int rsub = lane / LPR;
   char* base = a.pool + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + (int64_t)col * 16;
   const int64_t* rec = a.offsets + 2 * (int64_t)b * a.K;
-  // lane i < T holds the record of the tile's row i
-  int64_t rs = -1, rd = -1;
-  if (lane < T && h + lane < nk) {
-    rs = rec[2 * (h + lane)];
-    rd = rec[2 * (h + lane) + 1];
+  // register r of lane i holds the record of the tile's row r * 64 + i
+  int64_t rs[RPL], rd[RPL];
+#pragma unroll
+  for (int r = 0; r < RPL; ++r) {
+    const int t = r * 64 + lane;
+    rs[r] = rd[r] = -1;
+    if (t < T && h + t < nk) {
+      rs[r] = rec[2 * (h + t)];
+      rd[r] = rec[2 * (h + t) + 1];
+    }
   }
   // (waiting here too keeps the loop head free of a wait for the previous
   // tile's stores)
@@ -329,24 +335,35 @@ __global__ __launch_bounds__(kCompactThreads) void k_inplace_move(InplaceArgs a)
     int64_t dd[NI];
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int t = i * RPI + rsub;
-      const int64_t s = shfl64(rs, t);
-      dd[i] = shfl64(rd, t);
+      // row i * RPI + rsub of the tile; RPI divides 64, so its register is
+      // known at compile time
+      const int r = (i * RPI) / 64;
+      const int src = (i * RPI) % 64 + rsub;
+      const int64_t s = shfl64(rs[r], src);
+      dd[i] = shfl64(rd[r], src);
       if (s >= 0 && col_ok) v[i] = ld_stream(base + s);
     }
     // next tile's records, while this tile's rows are in flight
-    int64_t ns = -1, nd = -1;
-    const int jn = j0 + T + lane;
-    if (lane < T && jn < nk) {
-      ns = rec[2 * jn];
-      nd = rec[2 * jn + 1];
+    int64_t ns[RPL], nd[RPL];
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+      const int t = r * 64 + lane;
+      const int jn = j0 + T + t;
+      ns[r] = nd[r] = -1;
+      if (t < T && jn < nk) {
+        ns[r] = rec[2 * jn];
+        nd[r] = rec[2 * jn + 1];
+      }
     }
     wait_vmem();
 #pragma unroll
     for (int i = 0; i < NI; ++i)
       if (dd[i] >= 0 && col_ok) st_stream(base + dd[i], v[i]);
-    rs = ns;
-    rd = nd;
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+      rs[r] = ns[r];
+      rd[r] = nd[r];
+    }
   }
 }
 
@@ -364,10 +381,14 @@ hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_inplace_check, dim3(a.B), dim3(kInplaceThreads), 0, s, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.lanes_per_row == 64) return launch_move<64, 16>(a, s);
-  if (a.lanes_per_row == 16) return launch_move<16, 8>(a, s);
-  if (a.lanes_per_row == 4) return launch_move<4, 4>(a, s);
-  return hipErrorInvalidValue;
+  switch (a.lanes_per_row * 1000 + a.tile_ni) {
+    case 64016: return launch_move<64, 16>(a, s);
+    case 16008: return launch_move<16, 8>(a, s);
+    case 16016: return launch_move<16, 16>(a, s);
+    case 4004: return launch_move<4, 4>(a, s);
+    case 4016: return launch_move<4, 16>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace epikv

@@ -166,6 +166,7 @@ struct InplaceArgs {
   int32_t B, K, page_size, row_bytes, n_lk;
   int32_t lanes_per_row;                   // 64, 16 or 4 lanes share one row of a plane
   int32_t n_slices;                        // ceil(row_bytes / 16 / lanes_per_row)
+  int32_t tile_ni;                         // row loads per lane and tile
 };
 
 struct FillArgs {

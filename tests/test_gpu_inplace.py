@@ -45,12 +45,16 @@ def _expected(pool, pt, keeps, lengths):
 
 CASES = {
     # name: overrides of _run
-    # column slices of 64 B, 256 B and 1 KiB (the library picks the widest
-    # that still gives 2048 independent walks)
+    # column slices of 1 KiB and 256 B (the library picks the widest that
+    # still gives 2048 independent walks, with 16- and 32-row tiles), 256 B
+    # with 64-row tiles when there are fewer walks, and 64 B for rows under
+    # 256 B (64- and 256-row tiles)
     "narrow_slices": dict(lengths=[300, 90, 500], K=64),
     "mid_slices": dict(lengths=[300, 90, 500, 120, 260, 64, 65, 200], K=64,
                        L=16),
     "wide_slices": dict(lengths=list(range(64, 320, 8)), K=48, L=16),
+    "row128_many": dict(lengths=list(range(64, 320, 8)), K=48, L=16, H=1,
+                        d=64),
     "page1": dict(lengths=[150, 90], K=40, page=1),
     "page1024": dict(lengths=[2500, 600], K=300, page=1024),
     "hd64_h1": dict(lengths=[300, 200], K=64, H=1, d=64),
