@@ -81,6 +81,13 @@ typedef enum epikv_smoothing {
                                stream's first sample */
 } epikv_smoothing;
 
+/* How epikv_evict_step rebuilds the cache (epikv_step_io.in_place). */
+typedef enum epikv_compact_mode {
+  EPIKV_COMPACT_OUT_OF_PLACE = 0,  /* epikv_compact into fresh pages (App. H) */
+  EPIKV_COMPACT_IN_PLACE = 1,      /* epikv_compact_inplace */
+  EPIKV_COMPACT_REMAP = 2          /* epikv_compact_remap (table rewritten) */
+} epikv_compact_mode;
+
 #define EPIKV_MAX_BAND 32   /* band layers per call */
 #define EPIKV_MAX_WINDOW 256
 
@@ -396,11 +403,20 @@ typedef struct epikv_step_io {
   int32_t* seq_status;          /* [B] */
   void* workspace;
   size_t workspace_bytes;       /* >= epikv_workspace_bytes(cfg, chunk) */
-  int32_t in_place;             /* nonzero: compact with epikv_compact_inplace
-                                   on src/src_pt; dst and dst_pt are ignored,
-                                   scores always follow their rows in place,
-                                   dst_scores must be NULL or scores, and
-                                   dst_pos must equal src_pos (moved in place) */
+  int32_t in_place;             /* EPIKV_COMPACT_OUT_OF_PLACE (0): epikv_compact
+                                   from src/src_pt into dst/dst_pt.
+                                   EPIKV_COMPACT_IN_PLACE (1): compact with
+                                   epikv_compact_inplace on src/src_pt; dst
+                                   and dst_pt are ignored, scores always
+                                   follow their rows in place, dst_scores
+                                   must be NULL or scores, and dst_pos must
+                                   equal src_pos (moved in place).
+                                   EPIKV_COMPACT_REMAP (2): the same with
+                                   epikv_compact_remap: src_pt is rewritten
+                                   on the device, so it must point to
+                                   writable memory (and overlap neither
+                                   keep_idx, n_keep nor the workspace).
+                                   Other values: EPIKV_EINVAL_PARAM. */
 } epikv_step_io;
 
 /*

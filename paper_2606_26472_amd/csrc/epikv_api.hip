@@ -533,6 +533,23 @@ InplaceArgs inplace_args(const epikv_cfg* c, const epikv_pool* pool, const int32
   return a;
 }
 
+// The page table that epikv_compact_remap rewrites must not overlap what
+// the device reads while it is being rewritten.
+int check_remap_table(const epikv_cfg* c, const int32_t* pt, int64_t ld_pt, const int32_t* keep_idx,
+                      const int32_t* n_keep, const void* ws, size_t ws_bytes) {
+  const size_t pt_bytes = 4 * (size_t)c->batch * (size_t)ld_pt;
+  if (overlap(pt, pt_bytes, keep_idx, 4 * (size_t)c->batch * (size_t)c->budget) ||
+      overlap(pt, pt_bytes, n_keep, 4 * (size_t)c->batch) || overlap(pt, pt_bytes, ws, ws_bytes))
+    return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
+InplaceArgs remap_args(InplaceArgs a, int32_t* pt) {
+  a.remap = 1;
+  a.pt_out = pt;
+  return a;
+}
+
 __global__ void k_fill(FillArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -709,16 +726,13 @@ EPIKV_EXPORT int epikv_compact_remap(const epikv_cfg* cfg, const epikv_pool* poo
   int st = check_compact_inplace(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos, ld_s,
                                  workspace, workspace_bytes);
   if (st) return st;
-  const size_t pt_bytes = 4 * (size_t)cfg->batch * (size_t)ld_pt;
-  if (overlap(page_table, pt_bytes, keep_idx, 4 * (size_t)cfg->batch * (size_t)cfg->budget) ||
-      overlap(page_table, pt_bytes, n_keep, 4 * (size_t)cfg->batch) ||
-      overlap(page_table, pt_bytes, workspace, workspace_bytes))
-    return EPIKV_EALIAS;
-  InplaceArgs a = inplace_args(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos, ld_s,
-                               seq_status, workspace);
-  a.remap = 1;
-  a.pt_out = page_table;
-  return launched(launch_compact_inplace(a, stream));
+  st = check_remap_table(cfg, page_table, ld_pt, keep_idx, n_keep, workspace, workspace_bytes);
+  if (st) return st;
+  return launched(launch_compact_inplace(
+      remap_args(inplace_args(cfg, pool, page_table, ld_pt, keep_idx, n_keep, scores, pos, ld_s,
+                              seq_status, workspace),
+                 page_table),
+      stream));
 }
 
 EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io, hipStream_t stream) {
@@ -744,12 +758,16 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   // The scores are compacted only when the caller asks for them (out of
   // place); in place they always follow their rows.
   const float* src_scores = io->dst_scores ? io->scores : nullptr;
+  if (io->in_place < 0 || io->in_place > EPIKV_COMPACT_REMAP) return EPIKV_EINVAL_PARAM;
   if (io->in_place) {
     if (io->dst_scores && io->dst_scores != io->scores) return EPIKV_EALIAS;
     if (io->src_pos != io->dst_pos) return EPIKV_EALIAS;
     st = check_compact_inplace(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep,
                                io->scores, io->dst_pos, io->ld_s, ws_offsets,
                                compact_ws_bytes(cfg));
+    if (!st && io->in_place == EPIKV_COMPACT_REMAP)
+      st = check_remap_table(cfg, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep,
+                             io->workspace, io->workspace_bytes);
   } else {
     st = check_compact(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt,
                        io->ld_dst_pt, io->keep_idx, io->n_keep, src_scores, io->dst_scores,
@@ -791,11 +809,13 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
     st = launched(launch_select(sel, stream));
     if (st) return st;
   }
-  if (io->in_place)
-    return launched(launch_compact_inplace(
-        inplace_args(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep, io->scores,
-                     io->dst_pos, io->ld_s, io->seq_status, ws_offsets),
-        stream));
+  if (io->in_place) {
+    InplaceArgs a = inplace_args(cfg, &io->src, io->src_pt, io->ld_src_pt, io->keep_idx, io->n_keep,
+                                 io->scores, io->dst_pos, io->ld_s, io->seq_status, ws_offsets);
+    // (with page remapping the caller's table is documented as rewritten)
+    if (io->in_place == EPIKV_COMPACT_REMAP) a = remap_args(a, const_cast<int32_t*>(io->src_pt));
+    return launched(launch_compact_inplace(a, stream));
+  }
   return launched(launch_compact(
       compact_args(cfg, &io->src, io->src_pt, io->ld_src_pt, &io->dst, io->dst_pt, io->ld_dst_pt,
                    io->keep_idx, io->n_keep, src_scores, io->dst_scores,

@@ -28,6 +28,7 @@ EPIKV_ELAUNCH = -7
 SEQ_OK = 0
 SEQ_BUDGET = 1
 SEQ_RANGE = 2
+COMPACT_OUT_OF_PLACE, COMPACT_IN_PLACE, COMPACT_REMAP = 0, 1, 2
 
 SIGNAL_HS = 0
 SIGNAL_LAGKV = 1
@@ -328,7 +329,7 @@ def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,
     io.keep_idx, io.n_keep = _ptr(keep_idx), _ptr(n_keep)
     io.seq_status = _ptr(seq_status)
     io.workspace, io.workspace_bytes = _ptr(workspace), int(workspace_bytes_)
-    io.in_place = 1 if in_place else 0
+    io.in_place = int(in_place)   # False/True, or a COMPACT_* mode
     return io
 
 

@@ -91,3 +91,19 @@ def tie_exempt_compare(keep_gpu, keep_ref, scores_ref, n_prefix, N, K, R,
         assert abs(s[i] - cut) <= bound, \
             f"position {i}: score {s[i]} vs cut {cut} (not a near tie)"
     return diff.size // 2
+
+
+def remap_expected(pool_np: np.ndarray, pt: np.ndarray, keeps, page: int):
+    """The oracle's in-place rebuild with page remapping of every sequence
+    of a host pool [L][2][n_pages][page][H*d], one sequence after the
+    other (None in `keeps`: sequence untouched).  Returns (pool, table)."""
+    import oracle as O
+    phys = pool_np.transpose(2, 3, 0, 1, 4).copy()     # [n_pages][page][...]
+    new_pt = pt.copy()
+    for b, keep in enumerate(keeps):
+        if keep is None:
+            continue
+        n = int(np.count_nonzero(pt[b] >= 0))
+        phys, row = O.compact_pages_remap(phys, pt[b, :n], keep, page)
+        new_pt[b, :n] = row
+    return phys.transpose(2, 3, 0, 1, 4), new_pt

@@ -352,6 +352,14 @@ def test_evict_step_in_place_validation(E):
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EALIAS
     io = _valid_io(E, A)
+    io.in_place = 3                      # not a compaction mode
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_PARAM
+    io = _valid_io(E, A)
+    io.in_place = E.COMPACT_REMAP        # the rewritten table on keep_idx
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS
+    io = _valid_io(E, A)
     io.in_place = 1
     io.n_prefix = None                   # the earlier stages still check
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \

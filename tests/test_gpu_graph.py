@@ -114,12 +114,14 @@ def test_graph_replays_match_eager(E, signal):
         torch.cuda.synchronize()
 
 
-def test_graph_in_place_step_and_token_scorer(E):
-    """The in-place step and the fused per-token scorer under capture: each
-    replay starts from the same inputs (the pool, scores and positions the
-    in-place step rewrites are restored first) and must match eager."""
+@pytest.mark.parametrize("mode", ["in_place", "remap"])
+def test_graph_in_place_step_and_token_scorer(E, mode):
+    """The in-place step (plain, or with page remapping) and the fused
+    per-token scorer under capture: each replay starts from the same inputs
+    (the pool, page table, scores and positions the in-place step rewrites
+    are restored first) and must match eager."""
     import torch
-    print("graph capture in place + score_tokens", flush=True)
+    print(f"graph capture in place ({mode}) + score_tokens", flush=True)
     g = synth.rng(801)
     B, C, K, page, L, H, d, D = 3, 16, 96, 16, 2, 8, 128, 256
     na, nb = 2, 2
@@ -152,12 +154,15 @@ def test_graph_in_place_step_and_token_scorer(E):
     ws_n = E.workspace_bytes(cfg, C)
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
     n_cached = dev(lengths.astype(np.int32))
+    pt0 = dev(pt)
+    pt_d = pt0.clone()
     io = E.make_step_io(
         C, hidden, D, C * D, n_cached,
         torch.zeros(B, dtype=torch.int32, device="cuda"),
-        E.pool_of(pool.view(L, 2, n_pages, page, H, d)), dev(pt), pt.shape[1],
+        E.pool_of(pool.view(L, 2, n_pages, page, H, d)), pt_d, pt.shape[1],
         E.Pool(), None, 0, scores, ld_s, st_in, st_out, keep, n_keep, status,
-        ws, ws_n, src_pos=pos, dst_pos=pos, in_place=True)
+        ws, ws_n, src_pos=pos, dst_pos=pos,
+        in_place=E.COMPACT_IN_PLACE if mode == "in_place" else E.COMPACT_REMAP)
 
     def work():
         E.epikv_evict_step(cfg, io)
@@ -165,7 +170,7 @@ def test_graph_in_place_step_and_token_scorer(E):
                              st_tok, tok_scores, ld_s)
 
     outs = (pool, scores, pos, keep, n_keep, status, st_out, st_tok,
-            tok_scores)
+            tok_scores, pt_d)
 
     def reset():
         for t in outs:
@@ -173,6 +178,7 @@ def test_graph_in_place_step_and_token_scorer(E):
         pool.copy_(pool0)
         scores.copy_(sc0)
         pos.copy_(pos0)
+        pt_d.copy_(pt0)
 
     def snapshot():
         torch.cuda.synchronize()
@@ -182,6 +188,8 @@ def test_graph_in_place_step_and_token_scorer(E):
     work()
     eager = snapshot()
     assert np.all(eager[5] == 0)
+    if mode == "remap":                  # the table changed
+        assert not np.array_equal(eager[9], pt)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):

@@ -14,7 +14,7 @@ import pytest
 
 import oracle as O
 import synth
-from harness import dev, gather_logical, host, scatter_logical
+from harness import dev, gather_logical, host, remap_expected, scatter_logical
 
 pytestmark = pytest.mark.gpu
 
@@ -189,12 +189,14 @@ def test_inplace_twice_in_a_row(E):
         cur_len = np.minimum(n_keep + 20, lengths)
 
 
-def test_inplace_step_small(E):
-    """epikv_evict_step with in_place set: the chunk's scores as the
-    oracle computes them, the selection of the GPU's fp32 scores, and the
-    pool and scores rebuilt in place."""
+@pytest.mark.parametrize("mode", ["in_place", "remap"])
+def test_inplace_step_small(E, mode):
+    """epikv_evict_step with in_place set (plain, or with page remapping):
+    the chunk's scores as the oracle computes them, the selection of the
+    GPU's fp32 scores, and the pool, the page table and the scores rebuilt
+    in place."""
     import torch
-    print("in-place evict_step", flush=True)
+    print(f"in-place evict_step ({mode})", flush=True)
     g = synth.rng(78)
     lengths = np.array([400, 150, 64])
     B, C, K, page, L, H, d, D, na, nb = 3, 32, 96, 16, 2, 8, 128, 256, 2, 2
@@ -231,13 +233,15 @@ def test_inplace_step_small(E):
     ws_n = E.workspace_bytes(cfg, C)
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
     desc = E.pool_of(pool_d.view(L, 2, used, page, H, d))
+    pt_d = dev(pt)
     io = E.make_step_io(
         C, [hd[l] for l in range(nband)], D, C * D,
         dev(lengths.astype(np.int32)), torch.zeros(B, dtype=torch.int32,
                                                    device="cuda"),
-        desc, dev(pt), pt.shape[1], E.Pool(), None, 0, scores, ld_s, st_in,
+        desc, pt_d, pt.shape[1], E.Pool(), None, 0, scores, ld_s, st_in,
         st_out, keep, n_keep, status, ws, ws_n, src_pos=pos_d,
-        dst_pos=pos_d, in_place=True)
+        dst_pos=pos_d, in_place=E.COMPACT_IN_PLACE if mode == "in_place"
+        else E.COMPACT_REMAP)
     # the chunk's fp32 scores as the step computes them: the same kernels
     # called one by one on the same inputs (deterministic, so bitwise equal)
     sig = torch.zeros((nband, B, C), device="cuda")
@@ -272,7 +276,12 @@ def test_inplace_step_small(E):
         exp_pos[b] = O.compact_rows_inplace(pos[b], ref)
     assert host(scores).tobytes() == exp_sc.tobytes()
     assert np.array_equal(host(pos_d), exp_pos)
-    exp_pool = _expected(pool, pt, keeps, lengths)
+    if mode == "in_place":
+        exp_pool, exp_pt = _expected(pool, pt, keeps, lengths), pt
+    else:
+        exp_pool, exp_pt = remap_expected(pool, pt, keeps, page)
+        print(f"  remapped pages: {[len(O.remap_pairs(k, page)) for k in keeps]}")
+    assert np.array_equal(host(pt_d), exp_pt)
     assert host(pool_d).tobytes() == exp_pool.tobytes()
 
 

@@ -15,7 +15,7 @@ import pytest
 
 import oracle as O
 import synth
-from harness import dev, gather_logical, host
+from harness import dev, gather_logical, host, remap_expected
 
 pytestmark = pytest.mark.gpu
 
@@ -61,20 +61,6 @@ def _keep_sets(kind, lengths, K, page, prefix, g):
         assert not isinstance(keep, str)
         keeps.append(np.asarray(keep, np.int64))
     return keeps
-
-
-def _expected(pool, pt, keeps, page):
-    """The oracle's rebuild of every sequence of a host pool
-    [L][2][n_pages][page][H*d], one sequence after the other."""
-    phys = pool.transpose(2, 3, 0, 1, 4).copy()        # [n_pages][page][...]
-    new_pt = pt.copy()
-    for b, keep in enumerate(keeps):
-        if keep is None:
-            continue
-        n = int(np.count_nonzero(pt[b] >= 0))
-        phys, row = O.compact_pages_remap(phys, pt[b, :n], keep, page)
-        new_pt[b, :n] = row
-    return phys.transpose(2, 3, 0, 1, 4), new_pt
 
 
 CASES = {
@@ -133,7 +119,7 @@ def _run(E, name, kind, lengths, K, L=2, H=8, d=128, page=16, prefix=None,
     n_pairs = [len(O.remap_pairs(k, page)) if k is not None else 0
                for k in keeps]
     print(f"  remapped pages per sequence: {n_pairs}", flush=True)
-    exp_pool, exp_pt = _expected(pool, pt, keeps, page)
+    exp_pool, exp_pt = remap_expected(pool, pt, keeps, page)
     exp_sc, exp_pos = sc.copy(), pos.copy()
     for b, keep in enumerate(keeps):
         if keep is not None:
@@ -230,7 +216,7 @@ def test_remap_twice_in_a_row(E):
         for b, k in enumerate(keeps):
             keep_idx[b, :k.size] = k
         n_keep = np.array([k.size for k in keeps], np.int32)
-        exp, exp_pt = _expected(exp, exp_pt, keeps, page)
+        exp, exp_pt = remap_expected(exp, exp_pt, keeps, page)
         E.epikv_compact_remap(cfg, desc, pt_d, pt.shape[1], dev(keep_idx),
                               dev(n_keep), None, None, 0, None, ws, ws_n)
         torch.cuda.synchronize()
