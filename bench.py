@@ -40,6 +40,14 @@ class Setup:
     pass
 
 
+# KV-vector signals of the Lag-KV workload: (C-ABI signal, keys, values,
+# lag-normalised)
+KV_SIGNALS = {"lagkv": ("SIGNAL_LAGKV", True, True, True),
+              "kv_key": ("SIGNAL_KV_KEY", True, False, False),
+              "kv_val": ("SIGNAL_KV_VAL", False, True, False),
+              "lagkv_key": ("SIGNAL_LAGKV_KEY", True, False, True)}
+
+
 def workload_kind(w: synth.Workload) -> str:
     """hs: a batch evicting after a chunk of new tokens; lagkv: the same
     with the Lag-KV signal; prefill: one trace scored in one shot; replay:
@@ -52,12 +60,13 @@ def workload_kind(w: synth.Workload) -> str:
     return "hs" if w.B > 1 else "replay"
 
 
-def algorithmic_bytes(w: synth.Workload, lengths, n_keep):
+def algorithmic_bytes(w: synth.Workload, lengths, n_keep, signal="lagkv"):
     """Bytes the step must move at least once (reads + writes), per stage.
 
     score   : hidden-state signal: the chunk's band-layer rows, h_prev read +
-              write, signal write; Lag-KV: the chunk's K and V rows at every
-              layer, the previous and new per-channel ranges, the per-plane
+              write, signal write; KV-vector signals: the chunk's K and/or V
+              rows at every layer, for the lag-normalised ones the previous
+              and new per-channel ranges of the used tensors, the per-plane
               partial sums written and read, signal write
     zscore  : signal read, carried ring read + write, scores write
     select  : every cached score read once, keep_idx written
@@ -71,9 +80,11 @@ def algorithmic_bytes(w: synth.Workload, lengths, n_keep):
     out = {}
     if w.signal == "lagkv":
         n_sig = 1
+        _, use_k, use_v, lag = KV_SIGNALS[signal]
+        used = (int(use_k) + int(use_v)) / 2
         rng_bytes = 2 * B * L * 2 * H * d * 4
-        out["score"] = (B * C * row + 2 * rng_bytes + 2 * B * 2 * L * C * 4
-                        + B * C * 4)
+        out["score"] = int(B * C * row * used + 2 * rng_bytes * used * lag
+                           + 2 * B * 2 * L * C * 4 + B * C * 4)
     else:
         n_sig = nb
         out["score"] = B * nb * (C * D * 2 + 2 * D * 2 + C * 4)
@@ -207,9 +218,10 @@ def _step_buffers(S, E, cfg, w, lengths, src_pt, dst_pt, n_src, n_dst, dev):
     S.dst = E.pool_of(S.dst_pool.view(L, 2, n_dst, page, H, d))
 
 
-def setup_lag(w: synth.Workload, E):
+def setup_lag(w: synth.Workload, E, signal="lagkv"):
     """The Lag-KV batch: B sequences of n_max cached tokens whose previous
-    chunk has been scored (so the step normalises by that chunk's range)."""
+    chunk has been scored (so the step normalises by that chunk's range),
+    scored with one of the KV-vector signals."""
     import torch
     S = Setup()
     g = synth.rng(w.seed)
@@ -235,7 +247,8 @@ def setup_lag(w: synth.Workload, E):
         f"dst {S.dst_pool.numel() * 2 / 1e9:.1f} GB filled in "
         f"{time.time() - t0:.1f}s")
     cfg = E.default_cfg(batch=B, n_layers=L, n_kv_heads=H, head_dim=d,
-                        page_size=page, signal=E.SIGNAL_LAGKV,
+                        page_size=page,
+                        signal=getattr(E, KV_SIGNALS[signal][0]),
                         smoothing=E.SMOOTH_MEAN, window=w.window, budget=K)
     S.cfg = cfg
     S.ld_s = N
@@ -632,10 +645,12 @@ def _oracle_rows(g, w, n):
     return np.concatenate([block] * ((n + 2047) // 2048))[:n]
 
 
-def cpu_baseline_lag(w: synth.Workload, S, budget_s: float = 12.0):
-    """The oracle on sequences of the Lag-KV step: the new chunk's
-    normalised variance signal against the previous chunk's range, the
-    trailing mean, the selection over all N tokens, the rebuild."""
+def cpu_baseline_lag(w: synth.Workload, S, budget_s: float = 12.0,
+                     signal="lagkv"):
+    """The oracle on sequences of the Lag-KV step: the new chunk's variance
+    signal (normalised against the previous chunk's range for the lag
+    variants), the trailing mean, the selection over all N tokens, the
+    rebuild."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_limits
@@ -647,15 +662,18 @@ def cpu_baseline_lag(w: synth.Workload, S, budget_s: float = 12.0):
     rows = _oracle_rows(g, w, N)
     prev = O.bf16_to_float64(synth.kv_rows(g, (C, L, 2, H, d)))
     new = O.bf16_to_float64(synth.kv_rows(g, (C, L, 2, H, d)))
-    _, q_prev, rng_prev = O.lagkv_chunk_scores(prev[:, :, 0], prev[:, :, 1],
-                                               None, np.zeros(0))
+    _, use_k, use_v, lag = KV_SIGNALS[signal]
+    _, q_prev, rng_prev = O.kv_chunk_scores(prev[:, :, 0], prev[:, :, 1],
+                                            use_k, use_v, lag, None,
+                                            np.zeros(0))
     old = S.scores.cpu().numpy().astype(np.float64)
     spent, done = 0.0, 0
     while done < w.B and spent < budget_s:
         scores = old[done, :N].copy()
         t0 = time.perf_counter()
-        s_new, _, _ = O.lagkv_chunk_scores(new[:, :, 0], new[:, :, 1],
-                                           rng_prev, q_prev[-(w.window - 1):])
+        s_new, _, _ = O.kv_chunk_scores(new[:, :, 0], new[:, :, 1], use_k,
+                                        use_v, lag, rng_prev,
+                                        q_prev[-(w.window - 1):])
         scores[N - C:] = s_new
         keep = O.select_keep(scores, 0, w.budget)
         kept = O.compact_rows(rows, keep)
@@ -667,8 +685,9 @@ def cpu_baseline_lag(w: synth.Workload, S, budget_s: float = 12.0):
     per_step = spent / done * w.B
     return {"value": 1.0 / per_step, "unit": "steps/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"{done} of {w.B} sequences of the same step (Lag-KV "
-                      f"score of the {C}-token chunk, select, compact of all "
+            "sample": f"{done} of {w.B} sequences of the same step "
+                      f"({signal} score of the {C}-token chunk, select, "
+                      f"compact of all "
                       f"{L} layers) timed on one core; scaled to the full "
                       f"batch ({spent:.1f}s measured)"}
 
@@ -770,6 +789,8 @@ def main():
     ap.add_argument("--online", action="store_true",
                     help="time the fused per-token scorer against the two "
                          "separate calls (one JSON line of its own)")
+    ap.add_argument("--signal", default="lagkv", choices=sorted(KV_SIGNALS),
+                    help="KV-vector signal of the lagkv_batch8 workload")
     ap.add_argument("--inplace", action="store_true",
                     help="compare the in-place and out-of-place rebuilds "
                          "(one JSON line of its own) instead of the step")
@@ -801,8 +822,14 @@ def main():
             "unit": "us", "n_gpus": 1, "data": "synthetic",
             "results": rows}), flush=True)
         return
-    S = {"hs": setup_hs, "replay": setup_hs, "lagkv": setup_lag,
-         "prefill": setup_prefill}[kind](w, E)
+    if args.signal != "lagkv" and kind != "lagkv":
+        print("--signal applies to the lagkv_batch8 workload", file=sys.stderr)
+        sys.exit(2)
+    if kind == "lagkv":
+        S = setup_lag(w, E, args.signal)
+    else:
+        S = {"hs": setup_hs, "replay": setup_hs,
+             "prefill": setup_prefill}[kind](w, E)
 
     # correctness guard: one step, every sequence must be OK with K kept
     E.epikv_evict_step(S.cfg, S.io)
@@ -811,7 +838,7 @@ def main():
     nk = S.n_keep.cpu().numpy()
     assert np.all(st == 0) and np.all(nk == np.minimum(S.lengths, w.budget)), \
         (st, nk)
-    ab = algorithmic_bytes(w, S.lengths, nk)
+    ab = algorithmic_bytes(w, S.lengths, nk, args.signal)
     if args.inplace:
         rows = inplace_report(E, S, w, args.steps)
         print(json.dumps({
@@ -888,11 +915,13 @@ def main():
               f"{w.n_layers} layers x {w.n_kv_heads} KV heads x {w.head_dim} "
               f"bf16 paged ({w.page_size}-token pages), HS bands 7-13/18-25, "
               f"z-score w={w.window}",
-        "lagkv": f"{w.name}: batched Lag-KV eviction step, B={w.B}, "
-                 f"N={w.n_max}, K={w.budget}, chunk of {w.chunk} new tokens "
-                 f"normalised by the previous chunk's range, {w.n_layers} "
-                 f"layers x {w.n_kv_heads} KV heads x {w.head_dim} bf16 "
-                 f"paged, trailing mean w={w.window}",
+        "lagkv": f"{w.name}: batched {args.signal} eviction step, "
+                 f"B={w.B}, N={w.n_max}, K={w.budget}, chunk of {w.chunk} "
+                 f"new tokens"
+                 + (" normalised by the previous chunk's range"
+                    if KV_SIGNALS[args.signal][3] else "")
+                 + f", {w.n_layers} layers x {w.n_kv_heads} KV heads x "
+                 f"{w.head_dim} bf16 paged, trailing mean w={w.window}",
         "replay": f"{w.name}: one sequence at its steady state, "
                   f"N={w.n_max} -> K={w.budget} after a {w.chunk}-token "
                   f"chunk, {w.n_layers} layers x {w.n_kv_heads} KV heads x "
@@ -941,9 +970,14 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample ...")
-        result["cpu_baseline"] = {"hs": cpu_baseline, "replay": cpu_baseline,
-                                  "lagkv": cpu_baseline_lag,
-                                  "prefill": cpu_baseline_prefill}[kind](w, S)
+        if kind == "lagkv":
+            result["cpu_baseline"] = cpu_baseline_lag(w, S,
+                                                      signal=args.signal)
+        else:
+            result["cpu_baseline"] = {"hs": cpu_baseline,
+                                      "replay": cpu_baseline,
+                                      "prefill": cpu_baseline_prefill}[kind](
+                                          w, S)
     print(json.dumps(result), flush=True)
 
 

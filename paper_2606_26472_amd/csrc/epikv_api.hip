@@ -71,7 +71,8 @@ size_t sig_bytes(const epikv_cfg* c, int chunk) {
   return align_up(4 * (size_t)n_sig(c) * (size_t)c->batch * (size_t)chunk);
 }
 
-// Row offset records [B][K][2] int64, then (in place) [B][2] int32.
+// Row offset records [B][K][2] int64, then (in place) [B][2] int32, then
+// (page remapping) [B][4][ceil(K / page_size)] int32.
 size_t compact_records_bytes(const epikv_cfg* c) {
   return align_up(16 * (size_t)c->batch * (size_t)c->budget);
 }
@@ -90,7 +91,9 @@ size_t compact_ws_bytes(const epikv_cfg* c) {
 // kLagRowsAhead rows per thread.
 int lag_splits(const epikv_cfg* c, int chunk) {
   const int rpp = kScoreThreads / (c->n_kv_heads * c->head_dim / 8);
-  const int64_t base = 2 * (int64_t)c->n_layers * c->batch;
+  // planes that do work: keys and values for Lag-KV, one tensor otherwise
+  const int planes = c->signal == EPIKV_SIGNAL_LAGKV ? 2 : 1;
+  const int64_t base = planes * (int64_t)c->n_layers * c->batch;
   int64_t s = (kLagWgWanted + base - 1) / base;
   const int64_t cap = std::max<int64_t>(1, chunk / (rpp * kLagRowsAhead));
   return (int)std::max<int64_t>(1, std::min(s, cap));
@@ -245,6 +248,9 @@ void lag_args(const epikv_cfg* c, int32_t chunk, const epikv_pool* pool, const i
   a->H = c->n_kv_heads;
   a->d = c->head_dim;
   a->page_size = c->page_size;
+  a->page_shift = -1;
+  for (int sh = 0; sh < 31; ++sh)
+    if ((1 << sh) == c->page_size) a->page_shift = sh;
   a->use_k = c->signal != EPIKV_SIGNAL_KV_VAL;
   a->use_v = c->signal == EPIKV_SIGNAL_LAGKV || c->signal == EPIKV_SIGNAL_KV_VAL;
   a->lag = uses_range(c->signal);

@@ -70,6 +70,7 @@ struct ScoreLagArgs {
   int64_t ld_pt;
   const int32_t* n_cached;
   int32_t B, C, L, H, d, page_size;
+  int32_t page_shift;                      // log2(page_size), or -1 if not a power of 2
   int32_t use_k, use_v, lag;               // tensors used; lag normalisation
   float eps;
   const int32_t* n_tok_in;

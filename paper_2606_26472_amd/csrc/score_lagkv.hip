@@ -52,6 +52,15 @@ __device__ __forceinline__ float group_sum(float v, int width) {
   return v;
 }
 
+// Channel ranges propagate NaN (IEEE minimum / maximum, one instruction on
+// gfx950), as a plain minimum over the chunk does.
+__device__ __forceinline__ float nan_min(float a, float b) {
+  return __builtin_elementwise_minimum(a, b);
+}
+__device__ __forceinline__ float nan_max(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);
+}
+
 __device__ __forceinline__ void unpack8(u32x4 w, float x[8]) {
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -60,6 +69,10 @@ __device__ __forceinline__ void unpack8(u32x4 w, float x[8]) {
   }
 }
 
+// WR: a row spans whole wavefronts (at least 64 16-byte columns), so the
+// row a wavefront works on, its page and its address are wave-uniform and
+// live in scalar registers; the vector units only do the arithmetic.
+template <bool LAG, bool WR>
 __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   extern __shared__ float lds[];
   const int tid = threadIdx.x;
@@ -72,7 +85,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int row_vec = HD >> 3;                 // 16-byte columns per row
   const int rpp = kScoreThreads / row_vec;     // rows per pass
   const int col = tid % row_vec;
-  const int ro = tid / row_vec;
+  const int ro = WR ? __builtin_amdgcn_readfirstlane(tid / row_vec) : tid / row_vec;
   const int gl = a.d >> 3;                     // lanes per head
   const int head = col / gl;
   const int row_bytes = HD * 2;
@@ -93,7 +106,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int32_t* pt = a.pt + (int64_t)b * a.ld_pt;
   const int64_t half = (int64_t)a.B * a.L * 2 * HD;
   const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
-  const bool fresh = a.lag && a.n_tok_in[b] <= 0;
+  const bool fresh = LAG && a.n_tok_in[b] <= 0;
   // Rows [r_lo, r_hi) of the chunk are this workgroup's.  The first chunk of
   // a stream is normalised by its own range, which needs every row before
   // any variance: one workgroup takes it whole.
@@ -109,14 +122,18 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   // Page of chunk row r (-1 for none), then the address of this thread's
   // column of the row (nullptr for none).  Split so that a batch of rows
   // issues all its page-table loads before any row load waits on one.
+  // (page sizes that are powers of two -- the usual case -- divide by a
+  // shift: a division costs some thirty instructions per row and lane)
   auto row_page = [&](int r) -> int {
     if (!seq_ok || r >= r_hi) return -1;
-    return pt[(start + r) / a.page_size];
+    const int pos = start + r;
+    return pt[a.page_shift >= 0 ? pos >> a.page_shift : pos / a.page_size];
   };
   auto row_ptr = [&](int r, int pg) -> const char* {
     if (pg < 0 || pg >= a.n_pages) return nullptr;
     const int pos = start + r;
-    return plane + (int64_t)pg * a.s_page + (int64_t)(pos % a.page_size) * row_bytes + col * 16;
+    const int slot = a.page_shift >= 0 ? pos & (a.page_size - 1) : pos % a.page_size;
+    return plane + (int64_t)pg * a.s_page + (int64_t)slot * row_bytes + col * 16;
   };
 
   float mn[8], mx[8], cmn[8], cmx[8];
@@ -140,8 +157,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
     for (int e = 0; e < 8; ++e) {
       float lo = cmb[col * 8 + e], hi = cmb[rpp * HD + col * 8 + e];
       for (int q = 1; q < rpp; ++q) {
-        lo = fminf(lo, cmb[q * HD + col * 8 + e]);
-        hi = fmaxf(hi, cmb[(rpp + q) * HD + col * 8 + e]);
+        lo = nan_min(lo, cmb[q * HD + col * 8 + e]);
+        hi = nan_max(hi, cmb[(rpp + q) * HD + col * 8 + e]);
       }
       cmn[e] = lo;
       cmx[e] = hi;
@@ -169,8 +186,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
         unpack8(raw[u], x);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          cmn[e] = fminf(cmn[e], x[e]);
-          cmx[e] = fmaxf(cmx[e], x[e]);
+          cmn[e] = nan_min(cmn[e], x[e]);
+          cmx[e] = nan_max(cmx[e], x[e]);
         }
       }
     }
@@ -180,7 +197,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
       mn[e] = cmn[e];
       mx[e] = cmx[e];
     }
-  } else if (a.lag) {
+  } else if (LAG) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       mn[e] = a.range_in[rbase + e];
@@ -225,11 +242,13 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
       float x[8];
       if (got[u]) {
         unpack8(raw[u], x);
+        if (LAG) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          cmn[e] = fminf(cmn[e], x[e]);
-          cmx[e] = fmaxf(cmx[e], x[e]);
-          if (a.lag) x[e] = (x[e] - mn[e]) * den[e];
+          for (int e = 0; e < 8; ++e) {
+            cmn[e] = nan_min(cmn[e], x[e]);
+            cmx[e] = nan_max(cmx[e], x[e]);
+            x[e] = (x[e] - mn[e]) * den[e];
+          }
         }
       } else {
 #pragma unroll
@@ -250,7 +269,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
     }
   }
   __syncthreads();
-  if (a.lag) {
+  if (LAG) {
     // this share's range of the chunk; the reduce kernel combines the shares
     combine();
     if (ro == 0) {
@@ -296,8 +315,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
     lo = a.prange[o];
     hi = a.prange[half + o];
     for (int sp = 1; sp < a.splits; ++sp) {
-      lo = fminf(lo, a.prange[sp * 2 * half + o]);
-      hi = fmaxf(hi, a.prange[sp * 2 * half + half + o]);
+      lo = nan_min(lo, a.prange[sp * 2 * half + o]);
+      hi = nan_max(hi, a.prange[sp * 2 * half + half + o]);
     }
   }
   a.range_out[o] = lo;
@@ -314,7 +333,16 @@ size_t lagkv_lds_bytes(int C, int H, int d) {
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
   const size_t lds = lagkv_lds_bytes(a.C, a.H, a.d);
-  hipLaunchKernelGGL(k_score_lagkv, dim3(2 * a.L, a.B, a.splits), dim3(kScoreThreads), lds, s, a);
+  const dim3 grid(2 * a.L, a.B, a.splits);
+  const bool wr = a.H * a.d / 8 >= 64;
+  if (a.lag && wr)
+    hipLaunchKernelGGL((k_score_lagkv<true, true>), grid, dim3(kScoreThreads), lds, s, a);
+  else if (a.lag)
+    hipLaunchKernelGGL((k_score_lagkv<true, false>), grid, dim3(kScoreThreads), lds, s, a);
+  else if (wr)
+    hipLaunchKernelGGL((k_score_lagkv<false, true>), grid, dim3(kScoreThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL((k_score_lagkv<false, false>), grid, dim3(kScoreThreads), lds, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int tok_blocks = (r.C + kScoreThreads - 1) / kScoreThreads;

@@ -33,9 +33,14 @@ def _sync():
 
 
 def _close(got, ref, tol=TOL):
+    """Largest relative error (floor 1); NaN must sit exactly where the
+    oracle has NaN (infinite error otherwise)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
-    err = np.abs(got - ref) / np.maximum(1.0, np.abs(ref))
+    if not np.array_equal(np.isnan(got), np.isnan(ref)):
+        return float("inf")
+    ok = ~np.isnan(ref)
+    err = np.abs(got[ok] - ref[ok]) / np.maximum(1.0, np.abs(ref[ok]))
     return float(err.max()) if err.size else 0.0
 
 
@@ -325,8 +330,21 @@ KV_SIGNALS = {  # name: (use keys, use values, lag-normalised)
 def test_kv_signals_match_oracle(E, signal, C):
     """Chunk lengths that split a plane's rows between several workgroups
     evenly (64), unevenly (37, 200) and not at all (1)."""
+    _run_kv(E, signal, C)
+
+
+@pytest.mark.parametrize("signal", ["lagkv", "kv_key"])
+def test_kv_signal_nan_propagates_as_in_the_oracle(E, signal):
+    """A NaN key channel of one token: its variance is NaN, the trailing
+    mean carries it through the window, and (lag-normalised) the chunk's
+    range of that channel is NaN, so the next chunk's signal is NaN too --
+    the plain minimum / maximum over the chunk the oracle takes."""
+    _run_kv(E, signal, 64, nan=True)
+
+
+def _run_kv(E, signal, C, nan=False):
     import torch
-    print(f"kv signal {signal} C={C}", flush=True)
+    print(f"kv signal {signal} C={C} nan={nan}", flush=True)
     use_k, use_v, lag = KV_SIGNALS[signal]
     sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
               "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
@@ -347,6 +365,8 @@ def test_kv_signals_match_oracle(E, signal, C):
         if Ns[b] > T:
             rows = np.concatenate([synth.kv_rows(g, (Ns[b] - T, L, 2, H * d)),
                                    rows])
+        if nan and b == 0:
+            rows[5, 1, 0, 7] = 0x7FC0        # token 5, layer 1, key channel 7
         tok.append(rows)
         pos = np.arange(Ns[b])
         pool[:, :, pt[b, pos // page], pos % page] = rows.transpose(1, 2, 0, 3)
@@ -390,14 +410,16 @@ def test_kv_signals_match_oracle(E, signal, C):
                 rng_out = secs["range"].numpy()
                 if use_k:
                     assert np.array_equal(rng_out[0, b][:, 0],
-                                          mn[:, 0].astype(np.float32))
+                                          mn[:, 0].astype(np.float32), equal_nan=True)
                     assert np.array_equal(rng_out[1, b][:, 0],
-                                          mx[:, 0].astype(np.float32))
+                                          mx[:, 0].astype(np.float32), equal_nan=True)
                 if use_v:
                     assert np.array_equal(rng_out[0, b][:, 1],
-                                          mn[:, 1].astype(np.float32))
+                                          mn[:, 1].astype(np.float32), equal_nan=True)
                     assert np.array_equal(rng_out[1, b][:, 1],
-                                          mx[:, 1].astype(np.float32))
+                                          mx[:, 1].astype(np.float32), equal_nan=True)
             prev_range[b] = own
             prior[b] = np.concatenate([prior[b], q_ref])[-(w - 1):]
+            if nan and b == 0 and j == 0:
+                assert np.isnan(got_s[b, lo:lo + C]).any()
         st = [st[1], st[0]]
