@@ -151,19 +151,12 @@ hipError_t launch_compact(const CompactArgs& args, hipStream_t s) {
   // 5% slower at eight workgroups per CU, and more planes per wavefront
   // slower still.)
   a.lk_per_block = 1;
-  a.planes_together = 1;
   a.blocks_per_seq = (a.K + kCompactWaves - 1) / kCompactWaves;
   hipLaunchKernelGGL(k_compact_resolve, dim3((a.K + kCompactThreads - 1) / kCompactThreads, a.B),
                      dim3(kCompactThreads), 0, s, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  switch (a.planes_together) {
-    case 1: return launch_nv<1>(a, s);
-    case 2: return launch_nv<2>(a, s);
-    case 4: return launch_nv<4>(a, s);
-    case 8: return launch_nv<8>(a, s);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_nv<1>(a, s);
 }
 
 }  // namespace epikv

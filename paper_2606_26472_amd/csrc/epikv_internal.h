@@ -140,7 +140,6 @@ struct CompactArgs {
   int32_t B, K, page_size, row_bytes, n_lk;
   // launch shape, chosen by launch_compact
   int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
-  int32_t planes_together;                 // planes loaded before storing (1,2,4,8)
   int32_t blocks_per_seq;                  // ceil(K / kCompactWaves)
 };
 
