@@ -175,7 +175,9 @@ size_t epikv_state_bytes(const epikv_cfg* cfg);
 int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
 
 /* Device scratch that epikv_evict_step (and epikv_score) needs for a chunk
- * of `chunk` new tokens per sequence.  0 for an invalid cfg or chunk < 1. */
+ * of `chunk` new tokens per sequence; for chunk = 0 (a step that only
+ * selects and compacts) the compaction's scratch.  0 for an invalid cfg or
+ * chunk < 0. */
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
 
 /* Device scratch of epikv_compact, epikv_compact_inplace and
@@ -424,6 +426,11 @@ typedef struct epikv_step_io {
  * `stream`, with no host synchronisation.  Equivalent to the four calls
  * above with the signal in the workspace; sequences with n_cached < chunk
  * are flagged RANGE by the select stage.
+ * chunk = 0 is the step of the online regime (Sec. 3.3), where every token
+ * was scored as it was generated (epikv_score_tokens) and its score is
+ * already frozen in `scores`: select and compact only.  hidden, state_in
+ * and state_out are then not used (may be NULL), and the workspace needs
+ * epikv_workspace_bytes(cfg, 0) = epikv_compact_workspace_bytes(cfg) bytes.
  */
 int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                      hipStream_t stream);

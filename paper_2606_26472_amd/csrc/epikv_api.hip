@@ -630,7 +630,8 @@ EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]) {
 }
 
 EPIKV_EXPORT size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk) {
-  if (check_cfg(cfg) || chunk < 1) return 0;
+  if (check_cfg(cfg) || chunk < 0) return 0;
+  if (chunk == 0) return compact_ws_bytes(cfg);  // a step without scoring
   return sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk) + compact_ws_bytes(cfg);
 }
 
@@ -745,22 +746,28 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   if (!io) return EPIKV_EINVAL_NULL;
   int st = check_cfg(cfg);
   if (st) return st;
-  if (io->chunk < 1) return EPIKV_EINVAL_SHAPE;
+  if (io->chunk < 0) return EPIKV_EINVAL_SHAPE;
+  // chunk 0: the chunk's scores are already frozen (scored token by token
+  // with epikv_score_tokens), so the step is selection + rebuild only
+  const bool scoring = io->chunk > 0;
   if (!io->workspace || io->workspace_bytes < epikv_workspace_bytes(cfg, io->chunk))
     return EPIKV_EWORKSPACE;
   if (!aligned16(io->workspace)) return EPIKV_EALIGN;
-  st = check_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
-                   io->ld_src_pt, io->n_cached, io->state_in, io->state_out,
-                   (float*)io->workspace, io->workspace, io->workspace_bytes, false);
-  if (st) return st;
-  st = check_zscore(cfg, io->chunk, (const float*)io->workspace, io->n_cached, io->state_in,
-                    io->state_out, io->scores, io->ld_s);
-  if (st) return st;
+  if (scoring) {
+    st = check_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
+                     io->ld_src_pt, io->n_cached, io->state_in, io->state_out,
+                     (float*)io->workspace, io->workspace, io->workspace_bytes, false);
+    if (st) return st;
+    st = check_zscore(cfg, io->chunk, (const float*)io->workspace, io->n_cached, io->state_in,
+                      io->state_out, io->scores, io->ld_s);
+    if (st) return st;
+  }
   st = check_select(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix, io->keep_idx, io->n_keep,
                     io->seq_status);
   if (st) return st;
   char* ws = (char*)io->workspace;
-  char* ws_offsets = ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk);
+  char* ws_offsets =
+      scoring ? ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk) : ws;
   // The scores are compacted only when the caller asks for them (out of
   // place); in place they always follow their rows.
   const float* src_scores = io->dst_scores ? io->scores : nullptr;
@@ -781,8 +788,8 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   }
   if (st) return st;
   const size_t ws_state = state_layout(cfg).total;
-  if (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
-      overlap(io->workspace, io->workspace_bytes, io->state_out, ws_state))
+  if (scoring && (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
+                  overlap(io->workspace, io->workspace_bytes, io->state_out, ws_state)))
     return EPIKV_EALIAS;
 
   float* sig = (float*)ws;
@@ -791,8 +798,12 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                                      io->keep_idx, io->n_keep, io->seq_status, io->chunk);
   const ZscoreArgs zs = zscore_args(cfg, io->chunk, sig, io->n_cached, io->state_in, io->state_out,
                                     io->scores, io->ld_s, nullptr);
-  bool fused = false;
-  if (cfg->signal == EPIKV_SIGNAL_HS) {
+  bool selected = false;  // the select stage is on the stream
+  if (!scoring) {
+    st = launched(launch_select(sel, stream));
+    if (st) return st;
+    selected = true;
+  } else if (cfg->signal == EPIKV_SIGNAL_HS) {
     const ScoreHsArgs hs =
         hs_args(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, io->state_in, io->state_out, sig);
     if (select_score_fusable(sel, hs)) {
@@ -803,10 +814,10 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
       if (st) return st;
       st = launched(launch_zscore(zs, stream));
       if (st) return st;
-      fused = true;
+      selected = true;
     }
   }
-  if (!fused) {
+  if (!selected) {
     st = run_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
                    io->ld_src_pt, io->n_cached, io->state_in, io->state_out, sig, partial, stream);
     if (st) return st;

@@ -95,7 +95,9 @@ def test_state_layout_sizes(E):
     assert off[4] - off[3] >= 4 * 2 * 8 * 32 * 2 * 8 * 128
     assert E.workspace_bytes(c, 128) >= 4 * 15 * 32 * 128
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
-    assert E.workspace_bytes(c, 0) == 0
+    assert E.workspace_bytes(c, -1) == 0
+    # a step that only selects and compacts needs the compaction's scratch
+    assert E.workspace_bytes(c, 0) == E.compact_workspace_bytes(c)
     # records, per-sequence info, four page arrays per sequence
     assert E.compact_workspace_bytes(c) == 16 * 32 * 4096 + 256 + 16 * 32 * 256
     assert E.workspace_bytes(c, 128) >= E.compact_workspace_bytes(c) \
@@ -237,9 +239,12 @@ def test_evict_step_validation(E):
     io.workspace_bytes = 1 << 20
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EINVAL_NULL                        # no state
-    io.chunk = 0
+    io.chunk = -1
     assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
         E.EPIKV_EINVAL_SHAPE
+    io.chunk = 0                                   # select + compact only:
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_NULL                        # no state needed, no scores
 
 
 def _valid_io(E, A):
@@ -262,6 +267,24 @@ def _valid_io(E, A):
     io.workspace = 512 * A
     io.workspace_bytes = 1 << 30
     return io
+
+
+@host_only
+def test_evict_step_without_scoring_skips_the_scorer_checks(E):
+    """chunk = 0: hidden states and scorer state are not used, so a state
+    pair that would be refused for a scoring step is not looked at; the
+    selection's arguments still are."""
+    L = E.lib()
+    c = E.default_cfg(batch=2, budget=256)
+    io = _valid_io(E, A)
+    io.state_out = io.state_in
+    io.n_prefix = None
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EALIAS                   # scoring step: the state pair
+    io.chunk = 0
+    io.hidden = None
+    assert L.epikv_evict_step(ctypes.byref(c), ctypes.byref(io), None) == \
+        E.EPIKV_EINVAL_NULL              # no scoring: the missing n_prefix
 
 
 @host_only

@@ -179,3 +179,81 @@ def test_state_checkpoint_and_resume(E):
     assert st2.tobytes() == full_st.tobytes()
     assert s1.tobytes() == full_s[:, :split].tobytes()
     assert s2.tobytes() == full_s[:, split:].tobytes()
+
+
+def test_online_step_equals_the_scoring_step(E):
+    """The online regime end to end: the C new tokens scored one call each
+    with epikv_score_tokens, then epikv_evict_step with chunk 0 (select and
+    rebuild only), give bit for bit the scores, kept sets, rebuilt cache and
+    scorer state of one epikv_evict_step that scores the same C tokens."""
+    import torch
+    print("online step vs scoring step", flush=True)
+    g = synth.rng(910)
+    B, C, K, page, L, H, d, D = 3, 16, 96, 16, 2, 8, 128, 256
+    na, nb = 2, 2
+    lengths = np.array([400, 150, 90])           # include the C new tokens
+    ld_s = int(lengths.max())
+    cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_band_a=na,
+                        n_band_b=nb, budget=K)
+    hid = dev(synth.f32_to_bf16_bits(
+        (g.standard_normal((na + nb, B, C, D)) * 2).astype(np.float32)))
+    sc0 = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc0[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    st = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8)
+    sec = E.state_sections(cfg, st)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C + 30).astype(np.int32))
+    sec["ring"][:] = torch.from_numpy(
+        (20 + g.standard_normal(tuple(sec["ring"].shape))).astype(np.float32))
+    sec["h_prev"][:] = torch.from_numpy(synth.f32_to_bf16_bits(
+        g.standard_normal(tuple(sec["h_prev"].shape)).astype(np.float32)
+    ).view(np.int16))
+    st0 = st.cuda()
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    src = dev(synth.random_bits16(g, (L, 2, n_src, page, H * d)))
+    S = E.pool_of(src.view(L, 2, n_src, page, H, d))
+    n_cached = dev(lengths.astype(np.int32))
+    n_prefix = dev(np.zeros(B, np.int32))
+    hidden = [hid[l] for l in range(na + nb)]
+
+    def run(online):
+        scores = dev(sc0)
+        dst = torch.zeros((L, 2, n_dst, page, H * d), dtype=torch.int16,
+                          device="cuda")
+        dsc = torch.full((B, ld_s), -7.0, device="cuda")
+        keep = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
+        nk = torch.zeros(B, dtype=torch.int32, device="cuda")
+        status = torch.zeros(B, dtype=torch.int32, device="cuda")
+        s_in, s_out = st0.clone(), torch.zeros_like(st0)
+        chunk = C
+        if online:
+            for t in range(C):
+                E.epikv_score_tokens(
+                    cfg, 1, [h[:, t:] for h in hidden], D, C * D,
+                    dev((lengths - C + t + 1).astype(np.int32)), s_in, s_out,
+                    scores, ld_s)
+                s_in, s_out = s_out, s_in
+            chunk, state = 0, s_in
+        ws_n = E.workspace_bytes(cfg, chunk)
+        ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+        io = E.make_step_io(
+            chunk, None if online else hidden, D, C * D, n_cached, n_prefix,
+            S, dev(src_pt), src_pt.shape[1],
+            E.pool_of(dst.view(L, 2, n_dst, page, H, d)), dev(dst_pt),
+            dst_pt.shape[1], scores, ld_s, None if online else s_in,
+            None if online else s_out, keep, nk, status, ws, ws_n,
+            dst_scores=dsc)
+        E.epikv_evict_step(cfg, io)
+        if not online:
+            state = s_out
+        torch.cuda.synchronize()
+        return [host(t).copy() for t in (scores, dst, dsc, keep, nk, status,
+                                         state)]
+
+    a = run(online=False)
+    b = run(online=True)
+    assert np.all(a[5] == 0) and np.all(a[4] == np.minimum(lengths, K))
+    for x, y, what in zip(a, b, ["scores", "cache", "compacted scores",
+                                 "keep_idx", "n_keep", "status", "state"]):
+        assert x.tobytes() == y.tobytes(), what
