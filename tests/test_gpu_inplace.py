@@ -285,14 +285,16 @@ def test_inplace_step_small(E, mode):
     assert host(pool_d).tobytes() == exp_pool.tobytes()
 
 
-def test_inplace_full_size_matches_out_of_place(E):
+@pytest.mark.parametrize("mode", ["in_place", "remap"])
+def test_inplace_full_size_matches_out_of_place(E, mode):
     """The 32-sequence batch (N 8k..32k, K = 4096, 32 layers): the step run
-    out of place, then in place on the same inputs.  Every sequence's
-    scores and positions, and sampled rows of every layer and K/V, agree;
-    sampled slots past n_keep keep their bytes."""
+    out of place, then in place (plain, or with page remapping) on the same
+    inputs.  Every sequence's scores and positions, and sampled rows of
+    every layer and K/V, agree; in place, sampled slots past n_keep keep
+    their bytes; with remapping the page table is the oracle's."""
     import torch
     import bench
-    print("in-place full size", flush=True)
+    print(f"in-place full size ({mode})", flush=True)
     w = synth.workload("ragged_batch32")
     S = bench.setup_hs(w, E)
     K, page = w.budget, w.page_size
@@ -317,21 +319,29 @@ def test_inplace_full_size_matches_out_of_place(E):
         S.n_prefix, S.src, S.src_pt, S.src_pt_host.shape[1], E.Pool(), None,
         0, S.scores, S.ld_s, S.state_in, S.state_out, S.keep_idx, S.n_keep,
         S.status, S.ws, S.ws_bytes, src_pos=S.src_pos, dst_pos=S.src_pos,
-        in_place=True)
+        in_place=E.COMPACT_IN_PLACE if mode == "in_place" else E.COMPACT_REMAP)
     E.epikv_evict_step(S.cfg, io)
     torch.cuda.synchronize()
     assert np.array_equal(host(S.keep_idx), keep)
     assert np.all(host(S.status) == 0)
     assert host(S.scores)[:, :K].tobytes() == host(S.dst_scores)[:, :K].tobytes()
     assert np.array_equal(host(S.src_pos)[:, :K], host(S.dst_pos)[:, :K])
-    moved = 0
+    new_pt = host(S.src_pt)
+    moved = pages = 0
     for b in range(w.B):
         moved += K - O.first_hole(keep[b])
-        assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, pick[b]),
+        if mode == "remap":
+            n = int(np.count_nonzero(S.src_pt_host[b] >= 0))
+            exp = O.page_table_after_remap(S.src_pt_host[b, :n], keep[b], page)
+            assert np.array_equal(new_pt[b, :n], exp), b
+            pages += len(O.remap_pairs(keep[b], page))
+        else:
+            assert np.array_equal(new_pt, S.src_pt_host)
+            assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, tail[b]),
+                                  tail_before[b]), b
+        assert np.array_equal(rows(S.src_pool, new_pt, b, pick[b]),
                               rows(S.dst_pool, S.dst_pt_host, b, pick[b])), b
-        assert np.array_equal(rows(S.src_pool, S.src_pt_host, b, tail[b]),
-                              tail_before[b]), b
-    print(f"  rows moved: {moved} of {w.B * K}")
+    print(f"  rows moved: {moved} of {w.B * K}; pages remapped: {pages}")
 
 
 def test_inplace_step_lagkv_matches_out_of_place(E):
