@@ -267,7 +267,7 @@ hipError_t launch_fill(const FillArgs& a, hipStream_t s);
 // Tunables the host layer validates against.
 constexpr int kScoreThreads = 256;
 constexpr int kScoreSeg = 32;            // tokens per score_hs workgroup (wide rows)
-constexpr int kScoreSegWave = 32;        // longest segment per score_hs wavefront (rows <= 4096)
+constexpr int kScoreSegWave = 64;        // longest segment per score_hs wavefront (rows <= 4096)
 constexpr int kScoreWavesWanted = 1024;  // shorten segments until this many wavefronts
 constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per lane)
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
