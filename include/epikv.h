@@ -5,8 +5,8 @@
  * Matrix" (Kolawole & Smith, arXiv 2606.26472):
  *
  *   score    hidden-state change g_l(t) = ||h_l(t) - h_l(t-1)||_2 at the band
- *            layers (Sec. 3.2, Eq. 1), or the lag-normalised K/V variance
- *            (Sec. 3.3, Lag-KV);
+ *            layers (Sec. 3.2, Eq. 1), or a K/V-vector variance (Sec. 3.3:
+ *            Lag-KV, KV-key, KV-val, lag-kv-key);
  *   zscore   causal trailing-window smoothing (Eq. 3 z-score, or the Eq. 2
  *            mean) and the band combination s = mean_A - mean_B (Fig. 1);
  *            the result is the token's frozen score (Sec. 3.3);
@@ -15,7 +15,12 @@
  *            Sec. 3.3, App. D);
  *   compact  rebuild the paged cache from the kept positions, in order, for
  *            every layer, K and V and KV head (App. H; the cache holds
- *            2*L*H*d_h scalars per token, Sec. 3.1).
+ *            2*L*H*d_h scalars per token, Sec. 3.1): into fresh pages, in
+ *            place, or in place with whole retained pages remapped.
+ *
+ * epikv_evict_step runs the four in one call; epikv_score_tokens fuses score
+ * and zscore for the online regime of scoring each token as it is generated
+ * (Sec. 3.3), after which the step only selects and compacts.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
