@@ -56,6 +56,7 @@ CASES = {
     "row128_many": dict(lengths=list(range(64, 320, 8)), K=48, L=16, H=1,
                         d=64),
     "page1": dict(lengths=[150, 90], K=40, page=1),
+    "page3": dict(lengths=[150, 91, 400], K=40, page=3),
     "page1024": dict(lengths=[2500, 600], K=300, page=1024),
     "hd64_h1": dict(lengths=[300, 200], K=64, H=1, d=64),
     "hd256_h8": dict(lengths=[300, 200], K=64, H=8, d=256),

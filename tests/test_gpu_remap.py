@@ -68,6 +68,7 @@ CASES = {
     "mixed_p16": dict(kind="mixed", lengths=[300, 90, 500, 64, 250], K=512),
     "mixed_p4": dict(kind="mixed", lengths=[200, 150, 77], K=512, page=4),
     "mixed_p1": dict(kind="mixed", lengths=[150, 90], K=512, page=1),
+    "mixed_p3": dict(kind="mixed", lengths=[200, 151, 77], K=512, page=3),
     "page1_select": dict(kind="select", lengths=[150, 90], K=40, page=1),
     "select_p16": dict(kind="select", lengths=[300, 90, 500, 120], K=64, L=8),
     "blocks_prefix": dict(kind="blocks", lengths=[640, 480], K=256,
