@@ -90,8 +90,13 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   const int head = col / gl;
   const int row_bytes = HD * 2;
 
-  float* vbuf = lds;                           // [C][H]
-  float* cmb = lds + a.C * a.H;                // [2][rpp][HD] range combine
+  // Per-(head, row) variances, [H][C + 1]: the padding puts the heads of
+  // one row, written together, in different banks, and the per-row sums
+  // read consecutive rows.  The range combine holds [2][rpp][8][row_vec]:
+  // lane = column, so every access is to consecutive words.
+  const int vld = a.C + 1;
+  float* vbuf = lds;
+  float* cmb = lds + a.H * vld;
   float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
   if ((kv == 0 && !a.use_k) || (kv == 1 && !a.use_v)) {
     if (sp == 0)
@@ -148,17 +153,17 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
     if (ro < rpp) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        cmb[ro * HD + col * 8 + e] = cmn[e];
-        cmb[(rpp + ro) * HD + col * 8 + e] = cmx[e];
+        cmb[(ro * 8 + e) * row_vec + col] = cmn[e];
+        cmb[((rpp + ro) * 8 + e) * row_vec + col] = cmx[e];
       }
     }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float lo = cmb[col * 8 + e], hi = cmb[rpp * HD + col * 8 + e];
+      float lo = cmb[e * row_vec + col], hi = cmb[(rpp * 8 + e) * row_vec + col];
       for (int q = 1; q < rpp; ++q) {
-        lo = nan_min(lo, cmb[q * HD + col * 8 + e]);
-        hi = nan_max(hi, cmb[(rpp + q) * HD + col * 8 + e]);
+        lo = nan_min(lo, cmb[(q * 8 + e) * row_vec + col]);
+        hi = nan_max(hi, cmb[((rpp + q) * 8 + e) * row_vec + col]);
       }
       cmn[e] = lo;
       cmx[e] = hi;
@@ -265,7 +270,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
         q = fmaf(dlt, dlt, q);
       }
       const float var = group_sum(q, gl) * inv_d;
-      if (live && (col % gl) == 0) vbuf[r * a.H + head] = got[u] ? var : 0.f;
+      if (live && (col % gl) == 0) vbuf[head * vld + r] = got[u] ? var : 0.f;
     }
   }
   __syncthreads();
@@ -283,7 +288,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
   }
   for (int r = r_lo + tid; r < r_hi; r += kScoreThreads) {
     float s = 0.f;
-    for (int h = 0; h < a.H; ++h) s += vbuf[r * a.H + h];
+    for (int h = 0; h < a.H; ++h) s += vbuf[h * vld + r];
     part[r] = s;
   }
 }
@@ -328,7 +333,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
 size_t lagkv_lds_bytes(int C, int H, int d) {
   const int HD = H * d;
   const int rpp = kScoreThreads / (HD / 8);
-  return (size_t)C * H * 4 + (size_t)2 * rpp * HD * 4;
+  return (size_t)(C + 1) * H * 4 + (size_t)2 * rpp * HD * 4;
 }
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
