@@ -322,12 +322,14 @@ def test_full_size_batched_step_sampled(E):
 
 
 @pytest.mark.parametrize("D,C,K", [(4096, 64, 256), (1000, 32, 512),
-                                   (4096, 100, 256)])
+                                   (4096, 128, 512), (4096, 100, 256),
+                                   (8192, 64, 512)])
 def test_step_equals_its_stages(E, D, C, K):
     """epikv_evict_step against its four stages called one by one on the
-    same inputs, bit for bit.  With C <= R (the first two cases) the step
-    selects and scores in one launch; with C > R (the third) it runs the
-    stages in order."""
+    same inputs, bit for bit.  With C <= R (the first three cases, the third
+    at C = R) the step selects and scores in one launch; with C > R, or rows
+    wider than the fused kernel's wavefront scorer takes (D = 8192), it runs
+    the stages in order."""
     import torch
     print(f"step vs stages D={D} C={C} K={K}", flush=True)
     g = synth.rng(950 + C)
