@@ -15,12 +15,18 @@
 //   move   one wavefront per (sequence, plane, column slice) walks the moved
 //          slots in ascending order, a tile of T rows at a time (16 to 256,
 //          deeper when there are few walks): it loads the tile's source rows,
-//          waits until every load has returned, then stores them.  A store to slot j can only overwrite a row that a
-//          slot <= j reads; slots of this tile have read theirs, and slots of
-//          later tiles read rows past the end of this tile (their sources
-//          are >= their own slots).  So one wavefront per column slice moves
-//          its bytes without any barrier or second copy, and different
-//          slices, planes and sequences touch disjoint bytes.
+//          waits until every load has returned, then stores them.  A store
+//          to slot j can only overwrite a row that a slot <= j reads; slots
+//          of this tile have read theirs, and slots of later tiles read rows
+//          past the end of this tile (their sources are >= their own slots).
+//          So one wavefront per column slice moves its bytes without any
+//          barrier or second copy, and different slices, planes and
+//          sequences touch disjoint bytes.
+//
+// With page remapping (epikv_compact_remap) the check kernel also rewrites
+// the page table so that whole retained pages change places instead of being
+// copied; the walk then skips their slots, and the ordering argument above
+// still holds for every row that moves (see remap_pages).
 #include "epikv_internal.h"
 
 namespace epikv {

@@ -13,14 +13,18 @@
 // Kernel 1: 256-thread workgroups per (layer, K|V) plane and sequence, each
 // streaming its share of the chunk's rows of that plane from the paged pool
 // (planes of an unused tensor only zero their partial sums; the first chunk
-// of a stream goes to one workgroup, which needs every row for the range).  Thread i owns
-// 8 channels (one 16-byte column) of a row and loads kLagRowsAhead rows
-// (page-table entries first, then the rows) before using any; the d/8 lanes
-// of one head reduce the variance with DPP row operations (two passes: mean,
-// then squared deviations), and per-(token, head) variances go to LDS.  The
-// normalisation multiplies by the reciprocal of the channel's range.  The
-// workgroup then writes per-token sums over its heads to
-// partial[b][plane][c].
+// of a stream goes to one workgroup, which needs every row for the range).
+// Thread i owns 8 channels (one 16-byte column) of a row and loads
+// kLagRowsAhead rows (page-table entries first, then the rows) before using
+// any; when a row spans whole wavefronts its index, page and address are
+// wave-uniform and computed with scalar instructions.  The d/8 lanes of one
+// head reduce the variance with DPP row operations (two passes: mean, then
+// squared deviations), and per-(token, head) variances go to LDS.  The
+// lag-normalised signals are a separate instantiation: it tracks the
+// chunk's per-channel range with IEEE minimum/maximum (a NaN propagates, as
+// in a plain minimum over the chunk) and multiplies by the reciprocal of the
+// previous range.  The workgroup then writes per-token sums over its heads
+// to partial[b][plane][c].
 // Kernel 2 sums the 2L planes in a fixed order and divides by L*H, and
 // combines the shares' channel ranges into the next chunk's reference.
 #include "epikv_internal.h"
