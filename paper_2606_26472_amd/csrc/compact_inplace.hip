@@ -90,8 +90,7 @@ __device__ __forceinline__ int find_kept(const int32_t* keep, int n, int64_t v) 
 // Runs inside the check kernel once keep_idx is known to be valid: rewrites
 // the destination half of the offset records of the moved slots, drops the
 // records of remapped pages (their rows do not move) and then rewrites the
-// table.  Per sequence, in the
-// workspace, indexed by destination page:
+// table.  Per sequence, in the workspace, indexed by destination page:
 //   src[m]  p if m is remapped, else -1
 //   npg[m]  the page slot m*page_size.. writes to (remapped: the table value)
 //   give[m] the rank, then the page, handed to position src[m] when that
