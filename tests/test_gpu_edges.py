@@ -44,6 +44,10 @@ CASES = {
     "band_b_empty": dict(nb=0, lengths=[300, 200]),
     "nan_hidden": dict(nan=True, lengths=[300, 200]),
     "single_layer_preset": dict(na=1, nb=1, lengths=[400, 150]),
+    "max_bands": dict(na=16, nb=16, lengths=[300, 200]),
+    # 1500 short sequences: grids sized by the batch, per-sequence loops
+    "many_sequences": dict(K=64, C=16, H=1, d=64,
+                           lengths=list(20 + (np.arange(1500) * 37) % 180)),
 }
 
 
