@@ -209,3 +209,83 @@ def test_graph_in_place_step_and_token_scorer(E, mode):
             assert a.tobytes() == b.tobytes(), rep
         junk = junk * 1.0001 + 1.0
         torch.cuda.synchronize()
+
+
+def _small_step(E, seed, B=3, C=16, K=96, L=2, H=8, d=128, D=256, page=16):
+    """Inputs and output buffers of one small eviction step (HS signal)."""
+    import torch
+    g = synth.rng(seed)
+    na, nb = 2, 2
+    lengths = np.array([400, 150, 200][:B])
+    ld_s = int(lengths.max())
+    cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_band_a=na,
+                        n_band_b=nb, budget=K)
+    hid = dev(synth.f32_to_bf16_bits(
+        (g.standard_normal((na + nb, B, C, D)) * 2).astype(np.float32)))
+    sc0 = np.zeros((B, ld_s), np.float32)
+    for b in range(B):
+        sc0[b, :lengths[b] - C] = synth.old_scores(g, int(lengths[b]) - C)
+    st_in = torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
+    E.epikv_state_init(cfg, st_in)
+    torch.cuda.synchronize()
+    sec = E.state_sections(cfg, st_in)
+    sec["n_tok"][:] = torch.from_numpy((lengths - C).astype(np.int32)).cuda()
+    src_pt, n_src = synth.page_tables(lengths, page, g)
+    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g)
+    src = dev(synth.random_bits16(g, (L, 2, n_src, page, H * d)))
+    out = dict(
+        scores=dev(sc0), dst=torch.zeros((L, 2, n_dst, page, H * d),
+                                         dtype=torch.int16, device="cuda"),
+        st_out=torch.zeros_like(st_in),
+        keep=torch.zeros((B, K), dtype=torch.int32, device="cuda"),
+        nk=torch.zeros(B, dtype=torch.int32, device="cuda"),
+        status=torch.zeros(B, dtype=torch.int32, device="cuda"))
+    ws_n = E.workspace_bytes(cfg, C)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    io = E.make_step_io(
+        C, [hid[l] for l in range(na + nb)], D, C * D,
+        dev(lengths.astype(np.int32)), dev(np.zeros(B, np.int32)),
+        E.pool_of(src.view(L, 2, n_src, page, H, d)), dev(src_pt),
+        src_pt.shape[1], E.pool_of(out["dst"].view(L, 2, n_dst, page, H, d)),
+        dev(dst_pt), dst_pt.shape[1], out["scores"], ld_s, st_in,
+        out["st_out"], out["keep"], out["nk"], out["status"], ws, ws_n)
+    io._keep_src = (src, hid, sc0)
+    return cfg, io, out, sc0
+
+
+def test_two_steps_on_two_streams_at_once(E):
+    """The library keeps no global state: two eviction steps with their own
+    buffers, enqueued on two streams without any synchronisation between
+    them, give bit for bit what each gives alone."""
+    import torch
+    print("two streams", flush=True)
+    runs = [_small_step(E, 1201), _small_step(E, 1202)]
+
+    def reset():
+        for cfg, io, out, sc0 in runs:
+            for k, t in out.items():
+                if k == "scores":
+                    t.copy_(torch.from_numpy(sc0).cuda())
+                else:
+                    t.zero_()
+        torch.cuda.synchronize()
+
+    def snap():
+        torch.cuda.synchronize()
+        return [[host(t).copy() for t in out.values()] for _, _, out, _ in runs]
+
+    reset()
+    for cfg, io, _, _ in runs:               # one after the other
+        E.epikv_evict_step(cfg, io)
+    alone = snap()
+    assert all(np.all(a[5] == 0) for a in alone)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(3):
+        reset()
+        for (cfg, io, _, _), s in zip(runs, streams):
+            with torch.cuda.stream(s):
+                E.epikv_evict_step(cfg, io)
+        got = snap()
+        for a, b in zip(got, alone):
+            for x, y in zip(a, b):
+                assert x.tobytes() == y.tobytes(), rep
