@@ -363,6 +363,141 @@ def test_lagkv_first_chunk_uses_own_range():
     assert s[0] == q[0]
 
 
+def _channel_grid(L, H, d):
+    """Per-(layer, K|V, head, channel) low ends and widths, dyadic so that
+    lo + r, lo + r/2 and lo + r/4 are exact; keys and values differ, so a
+    range taken from the wrong tensor, layer or head breaks the closed
+    forms below."""
+    l, kv, h, c = np.meshgrid(np.arange(L), np.arange(2), np.arange(H),
+                              np.arange(d), indexing="ij")
+    lo = 0.25 * c - l + 3.0 * kv - h
+    r = 1.0 + l + 2.0 * kv + 0.5 * h + 0.125 * c
+    return lo, r
+
+
+def _alternating(lo, r, even, odd):
+    """One token per (even, odd) pair: channel c of every (layer, K|V, head)
+    sits at lo + even*r for even c and lo + odd*r for odd c.  Returns keys
+    and values [1][L][H][d]."""
+    d = lo.shape[-1]
+    frac = np.where(np.arange(d) % 2 == 0, even, odd)
+    tok = lo + frac * r                      # [L][2][H][d]
+    return tok[None, :, 0], tok[None, :, 1]
+
+
+def _chunk(lo, r, *pairs):
+    ks, vs = zip(*(_alternating(lo, r, a, b) for a, b in pairs))
+    return np.concatenate(ks), np.concatenate(vs)
+
+
+@pytest.mark.parametrize("use_v", [True, False])
+def test_lag_signal_uses_the_previous_chunks_range(use_v):
+    """Sec. 3.3 / Table 1 ("lag-norm."): a chunk is normalised by the range
+    of the chunk before it, not by its own.  Three chained chunks, eps = 0,
+    every channel with its own range:
+      chunk 1: tokens alternating lo / lo+r and lo+r / lo -> own range
+               [lo, lo+r], values 0 / 1, variance 1/4 per tensor;
+      chunk 2: lo / lo+r/2 and back, under chunk 1's range -> 0 / 1/2,
+               variance 1/16 (its own range would give 1/4);
+      chunk 3: lo+r/4 / lo+r/2 and back, under chunk 2's range
+               [lo, lo+r/2] -> 1/2 / 1, variance 1/16 (chunk 1's range
+               would give 1/64, its own range 1/4).
+    Lag-KV sums the key and value variances, lag-kv-key has the key's only;
+    averaging over layers and heads keeps the per-head value."""
+    L, H, d = 2, 3, 8
+    lo, r = _channel_grid(L, H, d)
+    chunks = [_chunk(lo, r, (0.0, 1.0), (1.0, 0.0)),
+              _chunk(lo, r, (0.0, 0.5), (0.5, 0.0)),
+              _chunk(lo, r, (0.25, 0.5), (0.5, 0.25))]
+    n_t = 2.0 if use_v else 1.0
+    want_q = [n_t / 4, n_t / 16, n_t / 16]
+    prev, prior = None, np.zeros(0)
+    qs = []
+    for j, (k, v) in enumerate(chunks):
+        s, q, own = O.kv_chunk_scores(k, v, True, use_v, True, prev, prior,
+                                      O.SMOOTH_MEAN, W, 0.0)
+        assert np.array_equal(q, [want_q[j]] * 2), (j, q)
+        if use_v:
+            s2, q2, own2 = O.lagkv_chunk_scores(k, v, prev, prior,
+                                                O.SMOOTH_MEAN, W, 0.0)
+            assert np.array_equal(q2, q) and np.array_equal(s2, s)
+            assert all(np.array_equal(a, b) for a, b in zip(own, own2))
+        # the range handed on is this chunk's own, per channel
+        mn, mx = own
+        for t in range(2):
+            assert np.all(mn[:, 0] <= k[t]) and np.all(k[t] <= mx[:, 0])
+            assert np.all(mn[:, 1] <= v[t]) and np.all(v[t] <= mx[:, 1])
+        assert np.array_equal(mn[:, 0], np.minimum(k[0], k[1]))
+        assert np.array_equal(mx[:, 1], np.maximum(v[0], v[1]))
+        qs.extend(q)
+        # trailing-window mean (Eq. 2) of every sample so far
+        for i in range(2):
+            seen = qs[:2 * j + i + 1]
+            assert s[i] == pytest.approx(sum(seen) / len(seen), rel=1e-14)
+        prev, prior = own, np.concatenate([prior, q])
+    # The same chunks scored by their own ranges (what a missing lag would
+    # compute) differ from chunk 2 on.
+    for j in (1, 2):
+        k, v = chunks[j]
+        own_q = O.kv_chunk_scores(k, v, True, use_v, True, None, np.zeros(0),
+                                  O.SMOOTH_MEAN, W, 0.0)[1]
+        assert np.array_equal(own_q, [n_t / 4] * 2)
+    # and chunk 3 under chunk 1's range (a range not handed on) differs too
+    k, v = chunks[2]
+    stale = O.chunk_range(*chunks[0])
+    stale_q = O.kv_chunk_scores(k, v, True, use_v, True, stale, np.zeros(0),
+                                O.SMOOTH_MEAN, W, 0.0)[1]
+    assert np.array_equal(stale_q, [n_t / 64] * 2)
+
+
+@pytest.mark.parametrize("use_v", [True, False])
+def test_lag_signal_previous_range_with_eps_closed_form(use_v):
+    """A token alternating between the previous chunk's per-channel minimum
+    and maximum (width r = 4 in every channel, low ends all different):
+    0, r/(r+eps), ... -> variance (r/(r+eps))^2 / 4 per tensor, so Lag-KV
+    q = (r/(r+eps))^2 / 2 and lag-kv-key q = (r/(r+eps))^2 / 4.  Scored by
+    its own (degenerate) range the same token gives 0."""
+    L, H, d = 2, 2, 8
+    lo, _ = _channel_grid(L, H, d)
+    r = np.full(lo.shape, 4.0)
+    prev = _chunk(lo, r, (0.0, 1.0), (1.0, 0.0))
+    k, v = _chunk(lo, r, (0.0, 1.0))
+    rr = (4.0 / (4.0 + EPS)) ** 2
+    want = rr / 2 if use_v else rr / 4
+    q = O.kv_chunk_scores(k, v, True, use_v, True, O.chunk_range(*prev),
+                          np.zeros(0), O.SMOOTH_MEAN, W, EPS)[1]
+    assert q[0] == pytest.approx(want, rel=1e-14)
+    q_own = O.kv_chunk_scores(k, v, True, use_v, True, None, np.zeros(0),
+                              O.SMOOTH_MEAN, W, EPS)[1]
+    assert q_own[0] == 0.0
+    if use_v:
+        q2 = O.lagkv_chunk_scores(k, v, O.chunk_range(*prev), np.zeros(0),
+                                  O.SMOOTH_MEAN, W, EPS)[1]
+        assert q2[0] == pytest.approx(want, rel=1e-14)
+        assert O.lagkv_chunk_scores(k, v, None, np.zeros(0),
+                                    O.SMOOTH_MEAN, W, EPS)[1][0] == 0.0
+
+
+@pytest.mark.parametrize("use_k,use_v", [(True, False), (False, True),
+                                         (True, True)])
+def test_raw_kv_signals_ignore_any_range(use_k, use_v):
+    """KV-key / KV-val (and both) are variances of the raw vectors (Sec. 3.3,
+    Table 1): keys alternating +-2 and values +-1/2 give 4, 1/4 and 17/4
+    whatever range is passed, and the range handed on is still the
+    chunk's own."""
+    L, H, d = 3, 2, 8
+    sign = np.where(np.arange(d) % 2 == 0, 1.0, -1.0)
+    k = np.broadcast_to(2.0 * sign, (2, L, H, d)).copy()
+    v = np.broadcast_to(0.5 * sign, (2, L, H, d)).copy()
+    want = (4.0 if use_k else 0.0) + (0.25 if use_v else 0.0)
+    odd_range = (np.full((L, 2, H, d), -7.0), np.full((L, 2, H, d), 9.0))
+    for rng in (None, odd_range):
+        s, q, own = O.kv_chunk_scores(k, v, use_k, use_v, False, rng,
+                                      np.zeros(0), O.SMOOTH_MEAN, W, EPS)
+        assert np.array_equal(q, [want, want])
+        assert np.array_equal(own[0][:, 0], np.minimum(k[0], k[1]))
+
+
 def test_kv_variance_closed_forms():
     # Channels alternating +a / -a have population variance a^2 in every
     # head, whatever the layer: KV-key gives a_k^2, KV-val a_v^2, both
