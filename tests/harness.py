@@ -12,6 +12,18 @@ import synth
 
 DEV = "cuda"
 
+# Agreement with the oracle for floating-point results (the eviction step's
+# target: scores within 1e-3 relative).
+TOL = 1e-3
+# Quantities that are strictly positive -- the hidden-state change g, the
+# KV-vector signal q, and the mean / EMA / raw smoothing of such a signal
+# on its own (the KV-vector scores) -- are held to a pure relative error.
+POSITIVE = 0.0
+# Quantities that can sit at or near zero -- z-scores and band differences
+# s = mean_A - mean_B -- are held to 1e-3 relative above magnitude 1 and to
+# 1e-3 absolute below it.
+NEAR_ZERO = 1.0
+
 
 def torch():
     import torch as t
@@ -32,6 +44,48 @@ def host(t) -> np.ndarray:
     if a.dtype == np.int16:
         a = a.view(np.uint16)
     return a
+
+
+def rel_err(got, ref, floor=POSITIVE) -> float:
+    """Largest |got - ref| / max(floor, |ref|) over the elements.  With
+    floor 0 a reference of exactly 0 must be matched exactly (else the error
+    is infinite).  NaN must sit exactly where the reference has NaN."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    if not np.array_equal(np.isnan(got), np.isnan(ref)):
+        return float("inf")
+    ok = ~np.isnan(ref)
+    diff = np.abs(got[ok] - ref[ok])
+    den = np.maximum(floor, np.abs(ref[ok]))
+    if np.any((den == 0) & (diff != 0)):
+        return float("inf")
+    err = np.divide(diff, den, out=np.zeros_like(diff), where=den > 0)
+    return float(err.max()) if err.size else 0.0
+
+
+def idx(a):
+    """A host index array as a device int64 tensor."""
+    T = torch()
+    return T.from_numpy(np.asarray(a, dtype=np.int64)).to(DEV)
+
+
+def rebuilt_rows_equal(src_pool, src_pt_row, dst_pool, dst_pt_row, keep,
+                       page, first=0) -> bool:
+    """Every rebuilt row j >= first of one sequence, in every layer and K/V
+    plane, equals (bit for bit, on the device) the source row of position
+    keep[j].  Pools [L][2][n_pages][page][H*d] of 16-bit storage; compared
+    as integers, so NaN payloads count."""
+    T = torch()
+    keep = np.asarray(keep, dtype=np.int64)
+    j = np.arange(first, keep.size)
+    if j.size == 0:
+        return True
+    sv = src_pool.view(T.int16)
+    dv = dst_pool.view(T.int16)
+    src = sv[:, :, idx(src_pt_row[keep[j] // page]), idx(keep[j] % page), :]
+    dst = dv[:, :, idx(dst_pt_row[j // page]), idx(j % page), :]
+    return bool(T.equal(src, dst))
 
 
 def cfg_for(E, w: synth.Workload, **kw):

@@ -1,19 +1,21 @@
 """Parity of the Lag-KV batch and the one-shot long prefill at full size.
 
-Both run epikv_evict_step at the workload's real shape; the oracle checks
-the new chunk's scores (all of them for Lag-KV, sampled windows for the
-prefill), the retained set exactly against the oracle's ranking of the GPU's
-fp32 scores, and sampled rows of the rebuilt cache bit for bit.
+Both run epikv_evict_step at the workload's real shape.  The oracle checks
+every score the step writes (the new chunks' for Lag-KV, all 65,536 of the
+prefill, computed in float64 from the same bf16 rows), the retained set
+exactly against the oracle's ranking of the GPU's fp32 scores and against
+the oracle's own float64 ranking up to near-ties at the cut, and every row of
+the rebuilt cache bit for bit (compared on the device).
 """
 import numpy as np
 import pytest
 
 import oracle as O
 import synth
-from harness import dev, host
+from harness import (NEAR_ZERO, POSITIVE, TOL, dev, host, idx,
+                     rebuilt_rows_equal, rel_err, tie_exempt_compare)
 
 pytestmark = pytest.mark.gpu
-TOL = 1e-3
 
 
 @pytest.fixture(scope="module")
@@ -29,26 +31,6 @@ def E():
 def _sync():
     import torch
     torch.cuda.synchronize()
-
-
-def _rel_err(got, ref):
-    got = np.asarray(got, np.float64)
-    ref = np.asarray(ref, np.float64)
-    return float(np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref))))
-
-
-def _idx(a):
-    import torch
-    return torch.from_numpy(np.asarray(a, dtype=np.int64)).cuda()
-
-
-def _check_rebuilt_rows(E, src_pool, src_pt, dst_pool, dst_pt, keep, page,
-                        js):
-    """Rows js of the rebuilt cache equal the source rows they came from."""
-    kept = keep[js]
-    src = host(src_pool[:, :, _idx(src_pt[kept // page]), _idx(kept % page), :])
-    dst = host(dst_pool[:, :, _idx(dst_pt[js // page]), _idx(js % page), :])
-    assert np.array_equal(src, dst)
 
 
 def test_lagkv_batch_full_size(E):
@@ -78,8 +60,8 @@ def test_lagkv_batch_full_size(E):
         chunks.append(rows)
         for b in range(B):
             p = np.arange(lo, lo + C)
-            pool.view(torch.int16)[:, :, _idx(src_pt[b, p // page]),
-                                   _idx(p % page), :] = dev(
+            pool.view(torch.int16)[:, :, idx(src_pt[b, p // page]),
+                                   idx(p % page), :] = dev(
                 rows[b].reshape(C, L, 2, HD).transpose(1, 2, 0, 3))
     cfg = E.default_cfg(batch=B, n_layers=L, signal=E.SIGNAL_LAGKV,
                         smoothing=E.SMOOTH_MEAN, budget=K)
@@ -90,6 +72,7 @@ def test_lagkv_batch_full_size(E):
     sc = np.zeros((B, ld_s), np.float32)
     for b in range(B):
         sc[b, :N - 2 * C] = synth.old_scores(g, N - 2 * C)
+    old = sc[:, :N - 2 * C].astype(np.float64)
     scores = dev(sc)
     ws_n = E.workspace_bytes(cfg, C)
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
@@ -127,13 +110,17 @@ def test_lagkv_batch_full_size(E):
                                           np.zeros(0), O.SMOOTH_MEAN)
         s2, q2, _ = O.lagkv_chunk_scores(k2[:, :, 0], k2[:, :, 1], r1,
                                          q1[-63:], O.SMOOTH_MEAN)
-        assert _rel_err(gs[b, N - 2 * C:N - C], s1) <= TOL, b
-        assert _rel_err(gs[b, N - C:], s2) <= TOL, b
+        # Lag-KV scores are trailing means of variances: strictly positive
+        assert rel_err(gs[b, N - 2 * C:N - C], s1, POSITIVE) <= TOL, b
+        assert rel_err(gs[b, N - C:], s2, POSITIVE) <= TOL, b
         ref = O.select_keep(gs[b, :N], 0, K, R)
         assert np.array_equal(kh[b], ref), b
-        js = np.sort(g.choice(K, 32, replace=False))
-        _check_rebuilt_rows(E, pool.view(torch.int16), src_pt[b], dst,
-                            dst_pt[b], kh[b], page, js)
+        # the oracle's own float64 ranking, near-ties at the cut exempted
+        s64 = np.concatenate([old[b], s1, s2])
+        tie_exempt_compare(kh[b], O.select_keep(s64, 0, K, R), s64, 0, N, K,
+                           R)
+        assert rebuilt_rows_equal(pool, src_pt[b], dst, dst_pt[b], kh[b],
+                                  page), b
 
 
 def test_prefill_one_shot_full_size(E):
@@ -186,27 +173,31 @@ def test_prefill_one_shot_full_size(E):
     _sync()
     assert host(status)[0] == 0 and host(n_keep)[0] == K
     gs = host(scores)[0]
-    # sampled windows: the stream start (no predecessor, warm-up) and
-    # random later tokens; the oracle needs rows t-64 .. t of every layer
-    targets = list(range(0, 70)) + sorted(g.choice(np.arange(70, T), 24,
-                                                   replace=False).tolist())
-    targets.append(T - 1)
-    for t in targets:
-        lo = max(0, t - 64)
-        rows = O.bf16_to_float64(host(hidv[:, 0, lo:t + 1]))  # [n_band][n][D]
-        sm = np.zeros(w.n_band)
-        for l in range(w.n_band):
-            gl, has = O.residual_delta(rows[l], None)
-            if lo == 0:
-                sm[l] = O.smooth_stream(np.zeros(0), gl, has, O.SMOOTH_Z)[-1]
-            else:
-                # rows lo..t give samples lo+1..t: the full window of t
-                sm[l] = O.rolling_zscore(gl[1:])[-1]
-        s_ref = O.band_score(sm[:, None], na, nb)[0]
-        assert _rel_err([gs[t]], [s_ref]) <= TOL, t
+    # every token's float64 score: Eq. 1 over each band layer's rows in
+    # blocks (the last row of a block is the next block's predecessor), then
+    # the trailing-window z-score of the whole stream and the band
+    # combination
+    blk = 4096
+    sm = np.zeros((w.n_band, T))
+    for l in range(w.n_band):
+        gl = np.zeros(T)
+        has = np.zeros(T, dtype=bool)
+        before = None
+        for lo in range(0, T, blk):
+            rows = O.bf16_to_float64(host(hidv[l, 0, lo:lo + blk]))
+            gl[lo:lo + blk], has[lo:lo + blk] = O.residual_delta(rows, before)
+            before = rows[-1]
+        sm[l] = O.smooth_stream(np.zeros(0), gl, has, O.SMOOTH_Z)
+        print(f"  oracle band layer {l} done", flush=True)
+    s64 = O.band_score(sm, na, nb)
+    # band difference of z-scores: can sit at 0
+    assert rel_err(gs, s64, NEAR_ZERO) <= TOL
     R = O.default_recent(K)
     ref = O.select_keep(gs, 0, K, R)
     kh = host(keep)[0]
     assert np.array_equal(kh, ref)
-    js = np.sort(g.choice(K, 64, replace=False))
-    _check_rebuilt_rows(E, pool, src_pt[0], dstp, dst_pt[0], kh, page, js)
+    swaps = tie_exempt_compare(kh, O.select_keep(s64, 0, K, R), s64, 0, T, K,
+                               R)
+    print(f"  prefill: {swaps} near-tie swaps against the float64 ranking",
+          flush=True)
+    assert rebuilt_rows_equal(pool, src_pt[0], dstp, dst_pt[0], kh, page)

@@ -12,7 +12,7 @@ import pytest
 
 import oracle as O
 import synth
-from harness import dev, host
+from harness import NEAR_ZERO, TOL, dev, host, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -125,11 +125,9 @@ def _run_case(E, name, K=64, recent=-1, window=64, C=32, page=16, H=8, d=128,
         s_new, *_ = O.hs_chunk_scores(
             O.bf16_to_float64(hid[:, b]), O.bf16_to_float64(before[b]),
             prior, na, nb, O.SMOOTH_Z, window)
-        got = gs[b, N - Cc:N].astype(np.float64)
-        assert np.array_equal(np.isnan(got), np.isnan(s_new)), (name, b)
-        ok = ~np.isnan(s_new)
-        err = np.abs(got[ok] - s_new[ok]) / np.maximum(1.0, np.abs(s_new[ok]))
-        assert err.size == 0 or err.max() <= 1e-3, (name, b, err.max())
+        # band differences of z-scores (can sit at 0); NaN where the
+        # oracle has NaN
+        assert rel_err(gs[b, N - Cc:N], s_new, NEAR_ZERO) <= TOL, (name, b)
         ref = O.select_keep(gs[b, :N], int(prefix[b]), K, R)
         if isinstance(ref, str):
             assert sth[b] == E.SEQ_BUDGET and nk[b] == -1, (name, b)

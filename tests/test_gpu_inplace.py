@@ -14,7 +14,8 @@ import pytest
 
 import oracle as O
 import synth
-from harness import dev, gather_logical, host, remap_expected, scatter_logical
+from harness import (NEAR_ZERO, TOL, dev, gather_logical, host, rel_err,
+                     remap_expected, scatter_logical)
 
 pytestmark = pytest.mark.gpu
 
@@ -267,9 +268,8 @@ def test_inplace_step_small(E, mode):
         s_new, *_ = O.hs_chunk_scores(
             O.bf16_to_float64(hid[:, b]), O.bf16_to_float64(before[b]),
             prior, na, nb, O.SMOOTH_Z, w)
-        got = full[b, N - C:N].astype(np.float64)
-        err = np.abs(got - s_new) / np.maximum(1.0, np.abs(s_new))
-        assert err.max() <= 1e-3, (b, err.max())
+        # band differences of z-scores: can sit at 0
+        assert rel_err(full[b, N - C:N], s_new, NEAR_ZERO) <= TOL, b
         ref = O.select_keep(full[b, :N], 0, K, R)
         assert nk[b] == ref.size and np.array_equal(kh[b, :ref.size], ref), b
         keeps.append(ref)

@@ -12,7 +12,7 @@ import pytest
 
 import oracle as O
 import synth
-from harness import dev, host
+from harness import NEAR_ZERO, TOL, dev, host, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -88,8 +88,7 @@ def test_chunking_invariance_bitwise(E, mode):
             gl, has = O.residual_delta(O.bf16_to_float64(hid[l, b]), None)
             sm.append(O.smooth_stream(np.zeros(0), gl, has, omode))
         s64 = O.band_score(np.array(sm), na, nb)
-        err = np.abs(ref_s[b] - s64) / np.maximum(1.0, np.abs(s64))
-        assert err.max() <= 1e-3
+        assert rel_err(ref_s[b], s64, NEAR_ZERO) <= TOL
 
 
 def test_ema_online_matches_one_shot(E):
@@ -114,8 +113,24 @@ def test_ema_online_matches_one_shot(E):
             gl, has = O.residual_delta(O.bf16_to_float64(hid[l, b]), None)
             sm.append(O.smooth_stream(np.zeros(0), gl, has, O.SMOOTH_EMA))
         s64 = O.band_score(np.array(sm), na, nb)
-        assert np.max(np.abs(s1[b] - s64) / np.maximum(1.0, np.abs(s64))) \
-            <= 1e-3
+        assert rel_err(s1[b], s64, NEAR_ZERO) <= TOL
+
+
+def _oracle_stream(hid, na, nb, mode, window):
+    """Float64 frozen scores of every token of [n_band][B][T][D] streams
+    scored from their start (Eq. 1, then the smoothing `mode` per band
+    layer, then the band combination)."""
+    omode = {"z": O.SMOOTH_Z, "mean": O.SMOOTH_MEAN, "raw": O.SMOOTH_RAW,
+             "ema": O.SMOOTH_EMA}[mode]
+    n_band, B, T, _ = hid.shape
+    out = np.zeros((B, T))
+    for b in range(B):
+        sm = []
+        for l in range(n_band):
+            gl, has = O.residual_delta(O.bf16_to_float64(hid[l, b]), None)
+            sm.append(O.smooth_stream(np.zeros(0), gl, has, omode, window))
+        out[b] = O.band_score(np.array(sm), na, nb)
+    return out
 
 
 @pytest.mark.parametrize("mode", ["z", "mean", "raw", "ema"])
@@ -123,7 +138,10 @@ def test_ema_online_matches_one_shot(E):
 def test_score_tokens_equals_two_calls(E, mode, D):
     """epikv_score_tokens (one launch per call) against epikv_score +
     epikv_zscore on the same chunking: scores and carried state bitwise,
-    from a fresh stream and from a carried state (window 64 and 5)."""
+    from a fresh stream and from a carried state (window 64 and 5); and its
+    scores against the oracle's float64 scores of the same stream (Sec. 3.3:
+    a token's score is frozen when it is generated, so scoring a stream
+    call by call must give the scores of the whole stream)."""
     import torch
     print(f"fused per-token scoring {mode} D={D}", flush=True)
     g = synth.rng(903 + D)
@@ -138,6 +156,7 @@ def test_score_tokens_equals_two_calls(E, mode, D):
     for window in (64, 5):
         cfg = E.default_cfg(batch=B, hidden=D, n_band_a=na, n_band_b=nb,
                             smoothing=smode, window=window)
+        ref = _oracle_stream(hid, na, nb, mode, window)
         # a carried state: the stream's first 40 tokens scored beforehand
         _, st40 = _score_stream(E, cfg, hid[:, :, :40], [40])
         for chunks in ([1] * 12 + [7, 64, 1, 2, 64], [64, 64, 22]):
@@ -145,6 +164,8 @@ def test_score_tokens_equals_two_calls(E, mode, D):
             f = _score_stream(E, cfg, hid, chunks, fused=True)
             assert a[0].tobytes() == f[0].tobytes(), (window, chunks)
             assert a[1].tobytes() == f[1].tobytes(), (window, chunks)
+            # band differences: can sit at 0
+            assert rel_err(f[0], ref, NEAR_ZERO) <= TOL, (window, chunks)
         rest = hid[:, :, 40:]
         a = _score_stream(E, cfg, rest, [1] * 20 + [30, 60],
                           state0=torch.from_numpy(st40).cuda())
@@ -152,6 +173,9 @@ def test_score_tokens_equals_two_calls(E, mode, D):
                           state0=torch.from_numpy(st40).cuda())
         assert a[0].tobytes() == f[0].tobytes()
         assert a[1].tobytes() == f[1].tobytes()
+        # resumed from the carried state (ring, h_prev, EMA average): the
+        # scores of tokens 40.. of the uninterrupted stream
+        assert rel_err(f[0], ref[:, 40:], NEAR_ZERO) <= TOL, window
 
 
 def test_state_checkpoint_and_resume(E):

@@ -7,23 +7,23 @@
   went the other way cannot cascade.
 * A small ragged batch with prefill protection.
 * The batched step at its full size (32 sequences of 8k..32k tokens, K=4096,
-  32 layers) in the launch configuration the benchmark times, checked on
-  sampled sequences and rows.
+  32 layers) in the launch configuration the benchmark times: every
+  sequence's new scores and retained set, and every rebuilt row.
 
-Scores within 1e-3 (relative, floor 1); retained positions exact when the
-oracle ranks the GPU's own fp32 scores, and equal to the oracle's fp64
-ranking except for positions whose oracle scores sit within 1e-3 of the
-cut; compacted rows bit-exact.
+Scores within 1e-3 (relative, floor 1: band differences of z-scores can sit
+at 0); retained positions exact when the oracle ranks the GPU's own fp32
+scores, and equal to the oracle's fp64 ranking except for positions whose
+oracle scores sit within 1e-3 of the cut; compacted rows bit-exact.
 """
 import numpy as np
 import pytest
 
 import oracle as O
 import synth
-from harness import dev, host, tie_exempt_compare
+from harness import (NEAR_ZERO, TOL, dev, host, rebuilt_rows_equal, rel_err,
+                     tie_exempt_compare)
 
 pytestmark = pytest.mark.gpu
-TOL = 1e-3
 
 
 @pytest.fixture(scope="module")
@@ -42,9 +42,8 @@ def _sync():
 
 
 def _rel_err(got, ref):
-    got = np.asarray(got, np.float64)
-    ref = np.asarray(ref, np.float64)
-    return float(np.max(np.abs(got - ref) / np.maximum(1.0, np.abs(ref))))
+    """Scores of the hidden-state signal: band differences of z-scores."""
+    return rel_err(got, ref, NEAR_ZERO)
 
 
 def _oracle_stream_scores(hid_all, na, nb, w=64, eps=1e-6):
@@ -66,8 +65,8 @@ def _oracle_stream_scores(hid_all, na, nb, w=64, eps=1e-6):
 @pytest.mark.parametrize("name,steps,min_evict,row_sample,P,bands", [
     ("drift_replay", 16, 12, None, 0, "bands"),
     ("drift_replay", 16, 12, None, 64, "10/21"),
-    ("spike_replay", 40, 8, 256, 0, "bands"),
-    ("spike_replay", 40, 8, 256, 64, "bands")])
+    ("spike_replay", 128, 96, 256, 0, "bands"),
+    ("spike_replay", 128, 96, 256, 64, "bands")])
 def test_replay_matches_oracle(E, name, steps, min_evict, row_sample, P,
                                bands):
     """P: protected prefill tokens; bands: the 7-13 / 18-25 bands, or the
@@ -270,7 +269,7 @@ def test_small_batch_matches_oracle(E):
 # ---------------------------------------------------------------------------
 # The batched step at full size, launch configuration of the benchmark
 # ---------------------------------------------------------------------------
-def test_full_size_batched_step_sampled(E):
+def test_full_size_batched_step(E):
     import torch
     import bench
     print("full-size batched step", flush=True)
@@ -283,42 +282,43 @@ def test_full_size_batched_step_sampled(E):
     st = host(S.status)
     nk = host(S.n_keep)
     assert np.all(st == 0) and np.all(nk == w.budget)
-    # determinism: a second identical step gives identical bits
-    dst_sample = host(S.dst_pool[:, :, :64]).copy()
+    # determinism: a second identical step gives identical bits (the whole
+    # rebuilt pool, the kept sets and the carried state)
+    dst_first = S.dst_pool.clone()
     out_state = host(S.state_out).copy()
     E.epikv_evict_step(S.cfg, S.io)
     _sync()
     assert np.array_equal(host(S.keep_idx), keep1)
-    assert np.array_equal(host(S.dst_pool[:, :, :64]), dst_sample)
+    assert torch.equal(S.dst_pool, dst_first)
+    del dst_first
     assert np.array_equal(host(S.state_out), out_state)
 
     C, K, page = w.chunk, w.budget, w.page_size
     na, nb = len(w.band_a), len(w.band_b)
     R = O.default_recent(K)
-    g = synth.rng(901)
-    for b in [0, 7, 19, 31]:
+    dsc, dpos = host(S.dst_scores), host(S.dst_pos)
+    swaps = 0
+    for b in range(w.B):
         N = int(S.lengths[b])
         prior = [S.ring_host[b, l].astype(np.float64) for l in range(w.n_band)]
         s_new, *_ = O.hs_chunk_scores(
             O.bf16_to_float64(S.hidden_host[:, b]),
             O.bf16_to_float64(S.before_host[:, b]), prior, na, nb)
         assert _rel_err(gs[b, N - C:N], s_new) <= TOL, b
+        # older tokens' frozen scores are inputs: untouched
+        assert np.array_equal(gs[b, :N - C], S.old_scores[b]), b
         ref = O.select_keep(gs[b, :N], 0, K, R)
         assert np.array_equal(keep1[b], ref), b
         s64 = np.concatenate([S.old_scores[b].astype(np.float64), s_new])
-        tie_exempt_compare(keep1[b], O.select_keep(s64, 0, K, R), s64, 0, N,
-                           K, R)
-        # sampled rows of the rebuilt cache, every layer and K/V
-        js = np.sort(g.choice(K, 48, replace=False))
-        src_rows = host(S.src_pool[:, :, torch.from_numpy(
-            S.src_pt_host[b, ref[js] // page].astype(np.int64)).cuda(),
-            torch.from_numpy((ref[js] % page).astype(np.int64)).cuda(), :])
-        dst_rows = host(S.dst_pool[:, :, torch.from_numpy(
-            S.dst_pt_host[b, js // page].astype(np.int64)).cuda(),
-            torch.from_numpy((js % page).astype(np.int64)).cuda(), :])
-        assert np.array_equal(src_rows, dst_rows), b
-        assert np.array_equal(host(S.dst_scores)[b, :K], gs[b, ref])
-        assert np.array_equal(host(S.dst_pos)[b, :K], ref.astype(np.int32))
+        swaps += tie_exempt_compare(keep1[b], O.select_keep(s64, 0, K, R),
+                                    s64, 0, N, K, R)
+        # every row of the rebuilt cache, every layer and K/V
+        assert rebuilt_rows_equal(S.src_pool, S.src_pt_host[b], S.dst_pool,
+                                  S.dst_pt_host[b], ref, page), b
+        assert np.array_equal(dsc[b, :K], gs[b, ref])
+        assert np.array_equal(dpos[b, :K], ref.astype(np.int32))
+    print(f"full-size step: {swaps} near-tie swaps against the float64 "
+          "ranking", flush=True)
 
 
 @pytest.mark.parametrize("D,C,K", [(4096, 64, 256), (1000, 32, 512),
