@@ -651,6 +651,7 @@ def cpu_baseline(w: synth.Workload, S, budget_s: float = 12.0):
         limiter.unregister()
     per_step = spent / done * w.B
     return {"value": 1.0 / per_step, "unit": "steps/s", "cores": 1,
+            "host_cores": os.cpu_count(),
             "kind": "oracle",
             "sample": f"{done} of {w.B} sequences of the same step (score, "
                       f"select, compact of all 32 layers) timed on one core; "
@@ -704,6 +705,7 @@ def cpu_baseline_lag(w: synth.Workload, S, budget_s: float = 12.0,
         limiter.unregister()
     per_step = spent / done * w.B
     return {"value": 1.0 / per_step, "unit": "steps/s", "cores": 1,
+            "host_cores": os.cpu_count(),
             "kind": "oracle",
             "sample": f"{done} of {w.B} sequences of the same step "
                       f"({signal} score of the {C}-token chunk, select, "
@@ -743,6 +745,7 @@ def cpu_baseline_prefill(w: synth.Workload, S, sample_tokens: int = 2048):
         limiter.unregister()
     per_step = t_score + t_rest
     return {"value": 1.0 / per_step, "unit": "steps/s", "cores": 1,
+            "host_cores": os.cpu_count(),
             "kind": "oracle",
             "sample": f"scores of the first {sample_tokens} of {T} tokens "
                       f"timed and scaled to the trace, plus the selection "
@@ -750,24 +753,64 @@ def cpu_baseline_prefill(w: synth.Workload, S, sample_tokens: int = 2048):
                       f"one core ({t_score + t_rest:.1f}s estimated)"}
 
 
+def _copy_probe_lib():
+    """The streaming-copy probe (libcopyprobe.so, built beside libepikv.so):
+    plain device copies in several launch shapes."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2606_26472_amd", "libcopyprobe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run "
+                           "python -m paper_2606_26472_amd.build")
+    lib = ctypes.CDLL(path)
+    lib.copy_probe.restype = ctypes.c_int
+    lib.copy_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    lib.copy_probe_variants.restype = ctypes.c_int
+    lib.copy_probe_name.restype = ctypes.c_char_p
+    lib.copy_probe_name.argtypes = [ctypes.c_int]
+    return lib
+
+
 def copy_ceiling(n_bytes: int = 4 << 30, reps: int = 5):
-    """Device-to-device copy bandwidth (read + write bytes / time) of a plain
-    torch copy of n_bytes: the practical streaming ceiling on this GPU."""
+    """Practical streaming ceiling of this GPU: the fastest of the copy
+    probe's launch shapes copying one contiguous n_bytes buffer (read +
+    write bytes / time, HIP events on the launch stream), and torch's own
+    copy for reference.  Returns (best GB/s, its ms, its shape, every
+    shape's GB/s)."""
     import torch
+    lib = _copy_probe_lib()
     a = torch.empty(n_bytes // 2, dtype=torch.int16, device="cuda")
     a.fill_(1)
     b = torch.empty_like(a)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
-    ev[0].record()
-    for i in range(reps):
-        b.copy_(a)
-        ev[i + 1].record()
-    torch.cuda.synchronize()
-    ms = np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    def timed(fn):
+        fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for i in range(reps):
+            fn()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([ev[i].elapsed_time(ev[i + 1])
+                              for i in range(reps)]))
+
+    shapes = {}
+    for v in range(lib.copy_probe_variants()):
+        def run(v=v):
+            rc = lib.copy_probe(a.data_ptr(), b.data_ptr(), n_bytes, v, sh)
+            if rc != 0:
+                raise RuntimeError(f"copy probe shape {v} failed: {rc}")
+        ms = timed(run)
+        shapes[lib.copy_probe_name(v).decode()] = (
+            round(2 * n_bytes / (ms * 1e-3) / 1e9, 1), ms)
+    ms_torch = timed(lambda: b.copy_(a))
     del a, b
-    return 2 * n_bytes / (ms * 1e-3) / 1e9, float(ms)
+    best = max(shapes, key=lambda k: shapes[k][0])
+    gbps = {k: v[0] for k, v in shapes.items()}
+    gbps["torch copy_"] = round(2 * n_bytes / (ms_torch * 1e-3) / 1e9, 1)
+    return shapes[best][0], shapes[best][1], best, gbps
 
 
 COMPACT_SOURCES = ("paper_2606_26472_amd/csrc/compact.hip",)
@@ -784,17 +827,22 @@ def compact_source_hash() -> str:
 
 def traffic_from_profiles():
     """HBM bytes per epikv_compact call from the committed counter summary,
-    if it was taken on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", "compact_ragged_batch32_traffic.json")
+    if it was taken on the current kernel sources (else None), and where
+    the figure comes from."""
+    rel = os.path.join("profiles", "compact_ragged_batch32_traffic.json")
+    path = os.path.join(ROOT, rel)
     if not os.path.exists(path):
-        return None
+        return None, None
     try:
         rec = json.load(open(path))
         if rec.get("kernel_sha256") != compact_source_hash():
-            return None
-        return rec.get("bytes_per_launch")
+            return None, None
+        return rec.get("bytes_per_launch"), (
+            f"{rel}: FETCH_SIZE + WRITE_SIZE counters of an earlier run on "
+            f"the same compaction source (sha256 "
+            f"{rec['kernel_sha256'][:16]}), not measured in this run")
     except Exception:
-        return None
+        return None, None
 
 
 def main():
@@ -916,8 +964,9 @@ def main():
                                           for k, v in stage_ms.items()))
     if args.stages_only:
         ms_step = stage_wall
-    copy_gbps, copy_ms = copy_ceiling()
-    log(f"[bench] device copy of 4 GiB: {copy_ms:.3f} ms = {copy_gbps:.0f} GB/s")
+    copy_gbps, copy_ms, copy_shape, copy_all = copy_ceiling()
+    log(f"[bench] streaming copy of 4 GiB: best {copy_ms:.3f} ms = "
+        f"{copy_gbps:.0f} GB/s ({copy_shape}); all shapes: {copy_all}")
     step_gbps = ab["step"] / (ms_step * 1e-3) / 1e9
     # the roofline is the dominant kernel's: the rebuild, or the scoring of
     # a one-shot prefill
@@ -927,8 +976,9 @@ def main():
                 "score": ("epikv_score (k_score_lagkv + k_lag_reduce)"
                           if kind == "lagkv" else
                           "epikv_score (k_score_hs_wave)")}[dom]
-    traffic = (traffic_from_profiles()
-               if (w.name, dom) == ("ragged_batch32", "compact") else None)
+    traffic, traffic_src = (traffic_from_profiles()
+                            if (w.name, dom) == ("ragged_batch32", "compact")
+                            else (None, None))
 
     descr = {
         "hs": f"{w.name}: batched eviction step, B={w.B} ragged N in "
@@ -985,7 +1035,9 @@ def main():
             "unit": "GB/s",
             "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
+            "traffic_source": traffic_src,
             "device_copy_gbps": round(copy_gbps, 1),
+            "device_copy_shape": copy_shape,
             "frac_of_device_copy": round(dom_gbps / copy_gbps, 4),
         },
     }

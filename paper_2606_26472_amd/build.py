@@ -1,4 +1,6 @@
-"""Build libepikv.so (gfx950) in-tree with hipcc.
+"""Build libepikv.so (gfx950) in-tree with hipcc, and beside it the
+benchmark's streaming-copy probe libcopyprobe.so (measurement only; not part
+of the eviction step's C ABI).
 
     python -m paper_2606_26472_amd.build
     python -m paper_2606_26472_amd.build --host-asan   # _build/asan/libepikv.so
@@ -25,6 +27,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libepikv.so")
+PROBE_LIB = os.path.join(PKG, "libcopyprobe.so")
+PROBE_SOURCES = ["copy_probe.hip"]
 
 SOURCES = ["epikv_api.hip", "score_hs.hip", "score_lagkv.hip", "zscore.hip",
            "select.hip", "compact.hip", "compact_inplace.hip", "score_tokens.hip",
@@ -76,16 +80,23 @@ def build(verbose: bool = False, host_asan: bool = False) -> str:
         _run(cmd)
         return obj
 
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    tmp = lib + ".tmp"
-    # (an instrumented library takes its sanitizer runtime from LD_PRELOAD)
-    cmd = [cc, "-shared", f"--offload-arch={ARCH}", "-fvisibility=hidden",
-           "-o", tmp, *objs]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    _run(cmd)
-    os.replace(tmp, lib)
+    def link(objs, target):
+        tmp = target + ".tmp"
+        # (an instrumented library takes its sanitizer runtime from
+        # LD_PRELOAD)
+        cmd = [cc, "-shared", f"--offload-arch={ARCH}", "-fvisibility=hidden",
+               "-o", tmp, *objs]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        _run(cmd)
+        os.replace(tmp, target)
+
+    todo = SOURCES + ([] if host_asan else PROBE_SOURCES)
+    with ThreadPoolExecutor(max_workers=min(8, len(todo))) as ex:
+        objs = dict(zip(todo, ex.map(compile_one, todo)))
+    link([objs[s] for s in SOURCES], lib)
+    if not host_asan:
+        link([objs[s] for s in PROBE_SOURCES], PROBE_LIB)
     return lib
 
 
