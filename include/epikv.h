@@ -27,7 +27,9 @@
  * - Pointers are device pointers unless marked "host".  The caller owns
  *   every buffer.  The library allocates nothing, keeps no global state,
  *   never synchronises, and enqueues its kernels on `stream` (0 = the null
- *   stream).  Calls on different streams are independent.
+ *   stream).  Calls on different streams are independent.  (The one
+ *   exception is epikv_evict_step_noalloc, whose scratch is a fixed
+ *   per-GPU array inside the library: see there.)
  * - bf16 tensors are passed as raw 16-bit storage.
  * - Return value: EPIKV_OK (0) or a negative epikv_status.  Every negative
  *   code except EPIKV_ELAUNCH is detected on the host before anything is
@@ -439,6 +441,34 @@ typedef struct epikv_step_io {
  */
 int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                      hipStream_t stream);
+
+/* Size of the scratch array behind epikv_evict_step_noalloc (per GPU). */
+#define EPIKV_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * epikv_evict_step_noalloc -- epikv_evict_step for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.
+ *
+ * Same arguments and results as epikv_evict_step, except that
+ * io->workspace and io->workspace_bytes are ignored: the step's scratch is
+ * a file-scope device array of EPIKV_NOALLOC_SCRATCH_BYTES (16 MiB) inside
+ * the library, one per GPU, held until the process ends.  A step that needs
+ * more than that (epikv_workspace_bytes(cfg, io->chunk) above the limit)
+ * returns EPIKV_EWORKSPACE before anything is enqueued.  Nothing is
+ * allocated.
+ *
+ * The first call on a device looks the array's device address up
+ * (hipGetSymbolAddress, with that device current); make it outside stream
+ * capture.  `stream` must belong to the calling thread's current device
+ * (else EPIKV_EINVAL_PARAM); the address lookup failing returns
+ * EPIKV_ELAUNCH.  Every call on one GPU shares its array, which keeps the
+ * last call's contents (the step writes what it reads, so nothing needs
+ * clearing): calls that overlap in time on one GPU -- on two streams, or
+ * from two threads -- race and must not be issued.
+ */
+int epikv_evict_step_noalloc(const epikv_cfg* cfg, const epikv_step_io* io,
+                             hipStream_t stream);
 
 #ifdef __cplusplus
 }

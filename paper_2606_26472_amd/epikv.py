@@ -47,7 +47,7 @@ EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_state_init", "epikv_score", "epikv_score_tokens",
             "epikv_zscore", "epikv_select", "epikv_compact",
             "epikv_compact_inplace", "epikv_compact_remap",
-            "epikv_evict_step")
+            "epikv_evict_step", "epikv_evict_step_noalloc")
 
 
 class EpikvError(RuntimeError):
@@ -132,6 +132,8 @@ def lib() -> ctypes.CDLL:
         "epikv_compact_remap": (ctypes.c_int, [cfgp, poolp, P, i64, P, P,
                                                P, P, i64, P, P, sz, P]),
         "epikv_evict_step": (ctypes.c_int, [cfgp, ctypes.POINTER(StepIO), P]),
+        "epikv_evict_step_noalloc": (ctypes.c_int,
+                                     [cfgp, ctypes.POINTER(StepIO), P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -336,6 +338,14 @@ def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,
 def epikv_evict_step(cfg: Cfg, io: StepIO, stream=None):
     _check(lib().epikv_evict_step(ctypes.byref(cfg), ctypes.byref(io),
                                   _stream(stream)), "epikv_evict_step")
+
+
+def epikv_evict_step_noalloc(cfg: Cfg, io: StepIO, stream=None):
+    """epikv_evict_step with the library's per-GPU scratch array
+    (io.workspace is ignored)."""
+    _check(lib().epikv_evict_step_noalloc(ctypes.byref(cfg), ctypes.byref(io),
+                                          _stream(stream)),
+           "epikv_evict_step_noalloc")
 
 
 # ---------------------------------------------------------------------------
