@@ -12,7 +12,6 @@
 
 namespace epikv {
 
-size_t lagkv_lds_bytes(int C, int H, int d);
 
 namespace {
 
@@ -86,30 +85,40 @@ size_t compact_ws_bytes(const epikv_cfg* c) {
          align_up(16 * (size_t)c->batch * (size_t)budget_pages(c));
 }
 
-// Workgroups sharing the rows of one (plane, sequence) in the KV-vector
+// Planes the KV-vector scorer reads: every (layer, K|V) for Lag-KV, the
+// layers of the one tensor otherwise.
+int lag_planes(const epikv_cfg* c) {
+  return (c->signal == EPIKV_SIGNAL_LAGKV ? 2 : 1) * c->n_layers;
+}
+
+// Workgroups sharing the rows of one (sequence, plane) in the KV-vector
 // scorer: enough for about kLagWgWanted workgroups, each keeping at least
-// kLagRowsAhead rows per thread.
+// kLagAhead rows per wavefront.
 int lag_splits(const epikv_cfg* c, int chunk) {
-  const int rpp = kScoreThreads / (c->n_kv_heads * c->head_dim / 8);
-  // planes that do work: keys and values for Lag-KV, one tensor otherwise
-  const int planes = c->signal == EPIKV_SIGNAL_LAGKV ? 2 : 1;
-  const int64_t base = planes * (int64_t)c->n_layers * c->batch;
-  int64_t s = (kLagWgWanted + base - 1) / base;
-  const int64_t cap = std::max<int64_t>(1, chunk / (rpp * kLagRowsAhead));
+  const int64_t base = (int64_t)lag_planes(c) * c->batch;
+  const int64_t s = (kLagWgWanted + base - 1) / base;
+  const int64_t cap = std::max<int64_t>(1, chunk / (kLagWaves * kLagAhead));
   return (int)std::max<int64_t>(1, std::min(s, cap));
 }
 
+// Partial channel ranges of the shares, when a plane's rows are split.
 size_t prange_bytes(const epikv_cfg* c, int chunk) {
-  if (!uses_range(c->signal)) return 0;
+  if (!uses_range(c->signal) || lag_splits(c, chunk) == 1) return 0;
   return align_up(4 * (size_t)lag_splits(c, chunk) * 2 * (size_t)c->batch * (size_t)c->n_layers *
                   2 * (size_t)c->n_kv_heads * (size_t)c->head_dim);
 }
 
-// Per-plane partial sums, then the per-split partial channel ranges.
+
+// Per-(sequence, plane, row segment, token) sums of the heads' variances,
+// then the shares' partial channel ranges.
+size_t plane_sums_bytes(const epikv_cfg* c, int chunk) {
+  const int segs = lagkv_segments(c->n_kv_heads, c->head_dim, uses_range(c->signal));
+  return align_up(4 * (size_t)c->batch * (size_t)lag_planes(c) * (size_t)segs * (size_t)chunk);
+}
+
 size_t partial_bytes(const epikv_cfg* c, int chunk) {
   if (!is_kv(c->signal)) return 0;
-  return align_up(4 * (size_t)c->batch * 2 * (size_t)c->n_layers * (size_t)chunk) +
-         prange_bytes(c, chunk);
+  return plane_sums_bytes(c, chunk) + prange_bytes(c, chunk);
 }
 
 int check_cfg(const epikv_cfg* c) {
@@ -201,7 +210,6 @@ int check_score(const epikv_cfg* c, int32_t chunk, const void* const* hidden, in
     if (st) return st;
     if (!page_table || !n_cached) return EPIKV_EINVAL_NULL;
     if (ld_pt < 1) return EPIKV_EINVAL_SHAPE;
-    if (lagkv_lds_bytes(chunk, c->n_kv_heads, c->head_dim) > (size_t)kLagMaxLds) return EPIKV_EINVAL_SHAPE;
     if (check_ws) {
       if (!ws || ws_bytes < sig_bytes(c, chunk) + partial_bytes(c, chunk)) return EPIKV_EWORKSPACE;
       if (!aligned16(ws)) return EPIKV_EALIGN;
@@ -251,27 +259,30 @@ void lag_args(const epikv_cfg* c, int32_t chunk, const epikv_pool* pool, const i
   a->page_shift = -1;
   for (int sh = 0; sh < 31; ++sh)
     if ((1 << sh) == c->page_size) a->page_shift = sh;
-  a->use_k = c->signal != EPIKV_SIGNAL_KV_VAL;
-  a->use_v = c->signal == EPIKV_SIGNAL_LAGKV || c->signal == EPIKV_SIGNAL_KV_VAL;
+  const bool use_k = c->signal != EPIKV_SIGNAL_KV_VAL;
+  const bool use_v = c->signal == EPIKV_SIGNAL_LAGKV || c->signal == EPIKV_SIGNAL_KV_VAL;
   a->lag = uses_range(c->signal);
+  a->n_planes = lag_planes(c);
+  a->two = use_k && use_v;
+  a->kv0 = use_k ? 0 : 1;
   a->eps = c->eps;
   a->n_tok_in = (const int32_t*)state_in;
   a->range_in = (const float*)((const char*)state_in + L.off[3]);
   a->range_out = (float*)((char*)state_out + L.off[3]);
   a->partial = partial;
   a->splits = lag_splits(c, chunk);
-  a->prange = a->lag ? (float*)((char*)partial + align_up(4 * (size_t)c->batch * 2 *
-                                                          (size_t)c->n_layers * (size_t)chunk))
-                     : nullptr;
+  a->prange = prange_bytes(c, chunk) ? (float*)((char*)partial + plane_sums_bytes(c, chunk))
+                                     : nullptr;
   r->partial = partial;
   r->sig = sig;
   r->B = c->batch;
   r->C = chunk;
-  r->n_lk = 2 * c->n_layers;
+  r->L = c->n_layers;
+  r->n_sums = a->n_planes * lagkv_segments(c->n_kv_heads, c->head_dim, a->lag);
   r->inv_count = 1.0f / (float)(c->n_layers * c->n_kv_heads);
   r->lag = a->lag;
-  r->use_k = a->use_k;
-  r->use_v = a->use_v;
+  r->use_k = use_k;
+  r->use_v = use_v;
   r->splits = a->splits;
   r->n_chan = c->n_layers * 2 * c->n_kv_heads * c->head_dim;
   r->prange = a->prange;

@@ -22,6 +22,11 @@ __device__ __forceinline__ void st_stream(void* p, u32x4 v) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// Buffer resources (gfx9 family): the fourth descriptor word of a raw
+// buffer, and the cache-policy bit of a non-temporal access.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+constexpr int kBufferNonTemporal = 2;
+
 // Sum over the 64 lanes of a wavefront with a fixed butterfly order, so the
 // result is identical on every lane and from run to run.
 __device__ __forceinline__ float wave_sum(float v) {
@@ -71,20 +76,22 @@ struct ScoreLagArgs {
   const int32_t* n_cached;
   int32_t B, C, L, H, d, page_size;
   int32_t page_shift;                      // log2(page_size), or -1 if not a power of 2
-  int32_t use_k, use_v, lag;               // tensors used; lag normalisation
+  int32_t lag;                             // lag normalisation
+  int32_t n_planes;                        // used planes: 2L (keys and values) or L
+  int32_t two, kv0;                        // both tensors used; else the one used
   float eps;
   const int32_t* n_tok_in;
   const float* range_in;                   // [2][B][L][2][H][d] (lag only)
   float* range_out;
-  float* partial;                          // [B][2L][C]
+  float* partial;                          // [B][n_planes][segments][C]
   int32_t splits;                          // workgroups sharing one plane's rows
   float* prange;                           // [splits][2][B][L][2][H][d] partial ranges
 };
 
 struct LagReduceArgs {
-  const float* partial;                    // [B][2L][C]
+  const float* partial;                    // [B][n_sums][C]
   float* sig;                              // [B][C]
-  int32_t B, C, n_lk;
+  int32_t B, C, L, n_sums;                 // n_sums = used planes x row segments
   float inv_count;                         // 1 / (L*H)
   int32_t lag, use_k, use_v, splits, n_chan;  // n_chan = L*2*H*d channels per sequence
   const float* prange;
@@ -278,9 +285,35 @@ constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per ga
 // Dynamic LDS the gather reserves (and never touches) to cap it at six
 // workgroups per CU: 160 KiB of LDS per CU on gfx950 / 24 KiB = 6.
 constexpr int kCompactLdsCap = 24 * 1024;
-constexpr int kLagMaxLds = 48 * 1024;
-constexpr int kLagRowsAhead = 8;         // chunk rows a Lag-KV thread loads before using them
-constexpr int kLagWgWanted = 1024;       // split a plane's rows until this many workgroups
+constexpr int kLagWaves = 8;             // wavefronts per KV-vector scorer workgroup
+constexpr int kLagThreads = kLagWaves * 64;
+constexpr int kLagAhead = 4;             // rows a KV-scorer wavefront loads before using them (even)
+constexpr int kLagWgWanted = 512;        // split a plane's rows until this many workgroups
+constexpr int kLagPtCache = 1024;        // page-table entries a KV-scorer workgroup keeps in LDS
+
+// KV-vector scorer: wavefronts per row (segments of 64 lanes x 8 or 16
+// channels), and LDS: the range combine's tree -- half as many slots of
+// [2][H*d] floats as partial ranges (row slots x rows per wavefront; the
+// broadcast reuses slot 0) -- then kLagPtCache page-table entries.
+// 16-byte columns per lane: 2 for the raw signals' rows of 1024 channels
+// or more, else 1.
+__host__ __device__ inline int lagkv_cpl(int H, int d, bool lag) {
+  return (!lag && H * d / 8 >= 128) ? 2 : 1;
+}
+__host__ __device__ inline int lagkv_segments(int H, int d, bool lag) {
+  const int row_vec = H * d / 8;
+  const int per = 64 * lagkv_cpl(H, d, lag);
+  return row_vec >= per ? row_vec / per : 1;
+}
+// (the tree exists for the lag-normalised signals only: one column per lane)
+__host__ __device__ inline int lagkv_tree_floats(int H, int d) {
+  const int HD = H * d;
+  const int row_vec = HD / 8;
+  const int n_part = row_vec >= 64 ? kLagWaves / lagkv_segments(H, d, true)
+                                   : kLagWaves * (64 / row_vec);
+  return (n_part > 1 ? n_part / 2 : 1) * 2 * HD;
+}
+size_t lagkv_lds_bytes(int H, int d, bool lag);
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
 

@@ -10,43 +10,62 @@
 // out as the next chunk's reference; the first chunk of a stream, with no
 // previous chunk, is normalised by its own range.
 //
-// Kernel 1: 256-thread workgroups per (layer, K|V) plane and sequence, each
-// streaming its share of the chunk's rows of that plane from the paged pool
-// (planes of an unused tensor only zero their partial sums; the first chunk
-// of a stream goes to one workgroup, which needs every row for the range).
-// Thread i owns 8 channels (one 16-byte column) of a row and loads
-// kLagRowsAhead rows (page-table entries first, then the rows) before using
-// any; when a row spans whole wavefronts its index, page and address are
-// wave-uniform and computed with scalar instructions.  The d/8 lanes of one
-// head reduce the variance with DPP row operations (two passes: mean, then
-// squared deviations), and per-(token, head) variances go to LDS.  The
-// lag-normalised signals are a separate instantiation: it tracks the
-// chunk's per-channel range with IEEE minimum/maximum (a NaN propagates, as
-// in a plain minimum over the chunk) and multiplies by the reciprocal of the
-// previous range.  The workgroup then writes per-token sums over its heads
-// to partial[b][plane][c].
-// Kernel 2 sums the 2L planes in a fixed order and divides by L*H, and
-// combines the shares' channel ranges into the next chunk's reference.
+// Kernel 1: one 512-thread workgroup per (sequence, used plane) -- a plane is
+// one (layer, K|V) of a used tensor, so signals of one tensor launch half as
+// many -- streaming the chunk's rows of that plane from the paged pool.  When
+// that gives too few workgroups to fill the GPU the rows are split between
+// `splits` workgroups, whose partial channel ranges the second kernel
+// combines; otherwise the workgroup writes the chunk's range itself.
+// A lane owns one 16-byte column = 8 channels of one head, so a head's
+// statistics reduce over d/8 lanes with DPP row operations.  A wavefront
+// takes a segment of 512 channels of a row (rows of 1024 channels: two
+// wavefronts per row, each writing its own partial sum), or several narrow
+// rows.  Each wavefront loads kLagAhead rows (page-table entries first, then
+// the rows) before it uses any; with row segments the row, its page and its
+// address are wave-uniform (scalar).
+//   Variance, one pass: the sum and the sum of squares over the head.  For
+//   the lag-normalised signals each channel is mapped to
+//   y = (x - mn) / (mx - mn + eps) - 1/2 (the shift keeps the sums of
+//   squares free of cancellation; a variance does not change under a
+//   shift); for the raw signals the packed bf16 words feed
+//   v_dot2_f32_bf16 directly (x0 + x1 and x0^2 + x1^2 in one instruction
+//   each, no unpacking).
+//   Range (lag-normalised, not the first chunk): IEEE minimum / maximum
+//   over the rows -- a NaN propagates, as in a plain minimum over the chunk
+//   -- with three-input instructions over pairs of rows; the wavefronts'
+//   ranges are combined through LDS in a fixed tree.
+//   First chunk of a stream (lag-normalised): a first pass over the rows
+//   finds the chunk's range, the second computes the variances with it.
+// Per (row, plane, segment) the sum of its heads' variances goes to
+// partial[b][plane][segment][c].
+// Kernel 2 sums the planes in a fixed order and divides by L*H, and (split
+// rows) combines the splits' channel ranges into the next chunk's reference.
 #include "epikv_internal.h"
 
 namespace epikv {
 namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of `width` lanes (8, 16 or 32), every lane of a
-// group ending with the same bits: each step adds two values that the
-// partner lane adds in the other order.  DPP moves within a row of 16 lanes
-// (rotations, half-row mirror, quad permutes) instead of LDS shuffles.
+// Sum over aligned groups of `width` lanes (2..32); every lane of a group
+// ends with the same bits (each step adds two values that the partner lane
+// adds in the other order).  Within a row of 16 lanes: DPP moves (quad
+// permutes, half-row mirror, rotations); across rows: a lane shuffle.
 __device__ __forceinline__ float group_sum(float v, int width) {
+  if (width == 2) return v + dpp<0xB1>(v);  // quad_perm [1,0,3,2]
+  if (width == 4) {
+    v += dpp<0xB1>(v);
+    return v + dpp<0x4E>(v);                // quad_perm [2,3,0,1]
+  }
   if (width == 8) {
     v += dpp<0x141>(v);  // row_half_mirror: lane i + lane 7-i
-    v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
-    v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
-    return v;
+    v += dpp<0x4E>(v);
+    return v + dpp<0xB1>(v);
   }
   v += dpp<0x128>(v);    // row_ror:8
   v += dpp<0x124>(v);    // row_ror:4
@@ -56,8 +75,17 @@ __device__ __forceinline__ float group_sum(float v, int width) {
   return v;
 }
 
-// Channel ranges propagate NaN (IEEE minimum / maximum, one instruction on
-// gfx950), as a plain minimum over the chunk does.
+// One 16-byte column of a row whose address is wave-uniform: a buffer
+// resource made for the row (scalar registers) and the lane's byte offset
+// as the only vector operand, so a row costs no vector address arithmetic.
+// The resource spans the row alone (offsets past it would read 0).
+// Non-temporal: each byte is read once.
+__device__ __forceinline__ u32x4 ld_row_nt(const char* row, uint32_t off, int row_bytes) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, row_bytes, kBufferRsrcWord3);
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kBufferNonTemporal);
+}
+
 __device__ __forceinline__ float nan_min(float a, float b) {
   return __builtin_elementwise_minimum(a, b);
 }
@@ -65,260 +93,428 @@ __device__ __forceinline__ float nan_max(float a, float b) {
   return __builtin_elementwise_maximum(a, b);
 }
 
-__device__ __forceinline__ void unpack8(u32x4 w, float x[8]) {
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    x[2 * k] = bf16_lo(w[k]);
-    x[2 * k + 1] = bf16_hi(w[k]);
-  }
-}
-
-// WR: a row spans whole wavefronts (at least 64 16-byte columns), so the
-// row a wavefront works on, its page and its address are wave-uniform and
-// live in scalar registers; the vector units only do the arithmetic.
-template <bool LAG, bool WR>
-__global__ __launch_bounds__(kScoreThreads) void k_score_lagkv(ScoreLagArgs a) {
+// LAG: lag-normalised signal.  WIDE: rows of at least 512 channels, split
+// into segments of 64 lanes x CPL 16-byte columns (8 * CPL channels per
+// lane), one segment per wavefront, so the row, its page and its address
+// are wave-uniform; narrower rows are shared by the lanes of one
+// wavefront, 64 / row_vec rows at a time (CPL = 1).  The raw signals take
+// two columns per lane for rows of 1024 channels or more, which halves the
+// per-row work (cross-lane sums, addressing) per channel; the
+// lag-normalised form keeps one (its per-channel range and normalisation
+// would not fit 128 registers with two).
+template <bool LAG, bool WIDE, int CPL>
+__global__ __launch_bounds__(kLagThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_score_lagkv(ScoreLagArgs a) {
+  constexpr int NCH = 8 * CPL;  // channels per lane
+  constexpr int AH = kLagAhead;  // rows per batch
+  static_assert(!(LAG && CPL > 1), "the lag-normalised form takes one column per lane");
   extern __shared__ float lds[];
   const int tid = threadIdx.x;
-  const int lk = blockIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int p = blockIdx.x;     // used plane
   const int b = blockIdx.y;
-  const int sp = blockIdx.z;                   // which share of the chunk's rows
-  const int layer = lk >> 1;
-  const int kv = lk & 1;
+  const int sp = blockIdx.z;    // share of the chunk's rows
+  const int layer = a.two ? p >> 1 : p;
+  const int kv = a.two ? (p & 1) : a.kv0;
   const int HD = a.H * a.d;
-  const int row_vec = HD >> 3;                 // 16-byte columns per row
-  const int rpp = kScoreThreads / row_vec;     // rows per pass
-  const int col = tid % row_vec;
-  const int ro = WR ? __builtin_amdgcn_readfirstlane(tid / row_vec) : tid / row_vec;
-  const int gl = a.d >> 3;                     // lanes per head
-  const int head = col / gl;
+  const int row_vec = HD >> 3;                    // 16-byte columns per row
+  const int segs = WIDE ? row_vec / (64 * CPL) : 1;  // wavefronts per row
+  const int lpr = WIDE ? 64 : row_vec;            // lanes per row segment
+  const int rpw = WIDE ? 1 : 64 / row_vec;        // rows per wavefront
+  const int seg = WIDE ? wave % segs : 0;         // this wavefront's segment
+  const int slot = WIDE ? wave / segs : wave;     // its row slot in the workgroup
+  const int rw = WIDE ? 0 : lane / lpr;           // this lane's row within the wavefront's
+  const int li = lane - rw * lpr;                 // lane within the segment
+  const int col = seg * 64 + li;                  // this lane's group of CPL columns
+  const int gw = a.d / NCH;                       // lanes per head
   const int row_bytes = HD * 2;
-
-  // Per-(head, row) variances, [H][C + 1]: the padding puts the heads of
-  // one row, written together, in different banks, and the per-row sums
-  // read consecutive rows.  The range combine holds [2][rpp][8][row_vec]:
-  // lane = column, so every access is to consecutive words.
-  const int vld = a.C + 1;
-  float* vbuf = lds;
-  float* cmb = lds + a.H * vld;
-  float* part = a.partial + ((int64_t)b * 2 * a.L + lk) * a.C;
-  if ((kv == 0 && !a.use_k) || (kv == 1 && !a.use_v)) {
-    if (sp == 0)
-      for (int r = tid; r < a.C; r += kScoreThreads) part[r] = 0.f;
-    return;
-  }
 
   const int N = a.n_cached[b];
   const int start = N - a.C;
   const bool seq_ok = start >= 0 && (int64_t)((N - 1) / a.page_size) < a.ld_pt;
-  const char* plane = a.base + (int64_t)layer * a.s_layer + (int64_t)kv * a.s_kv;
   const int32_t* pt = a.pt + (int64_t)b * a.ld_pt;
   const int64_t half = (int64_t)a.B * a.L * 2 * HD;
-  const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * 8;
+  // this lane's first channel in the [2][B][L][2][H][d] range layout
+  const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * NCH;
   const bool fresh = LAG && a.n_tok_in[b] <= 0;
-  // Rows [r_lo, r_hi) of the chunk are this workgroup's.  The first chunk of
-  // a stream is normalised by its own range, which needs every row before
-  // any variance: one workgroup takes it whole.
+  // this segment's row of partial sums [B][plane][segment][C]
+  float* part = a.partial + (((int64_t)b * a.n_planes + p) * segs + seg) * a.C;
+
+  // Rows [r_lo, r_hi) of the chunk are this workgroup's.  The first chunk
+  // of a stream needs every row for its range before any variance: the
+  // first share takes it whole.
   int r_lo = 0, r_hi = 0;
   if (fresh) {
     r_hi = sp == 0 ? a.C : 0;
   } else {
-    const int per = ((a.C + a.splits - 1) / a.splits + rpp - 1) / rpp * rpp;
+    const int per = (a.C + a.splits - 1) / a.splits;
     r_lo = min(a.C, sp * per);
     r_hi = min(a.C, r_lo + per);
   }
-
-  // Page of chunk row r (-1 for none), then the address of this thread's
-  // column of the row (nullptr for none).  Split so that a batch of rows
-  // issues all its page-table loads before any row load waits on one.
-  // (page sizes that are powers of two -- the usual case -- divide by a
-  // shift: a division costs some thirty instructions per row and lane)
-  auto row_page = [&](int r) -> int {
-    if (!seq_ok || r >= r_hi) return -1;
-    const int pos = start + r;
-    return pt[a.page_shift >= 0 ? pos >> a.page_shift : pos / a.page_size];
+  const int slots = kLagWaves / segs;                     // row slots of the workgroup
+  // Each row slot walks its own contiguous block of the share's rows, rpw
+  // rows per sweep (narrow rows: one per lane group), so consecutive rows
+  // of a wavefront mostly share a page.
+  const int per_slot = ((r_hi - r_lo + slots - 1) / slots + rpw - 1) / rpw * rpw;
+  const int s_lo = min(r_hi, r_lo + slot * per_slot);
+  const int s_hi = min(r_hi, s_lo + per_slot);
+  const int sweeps = (s_hi - s_lo + rpw - 1) / rpw;     // this wavefront's
+  auto row_of = [&](int it) { return s_lo + it * rpw + rw; };
+  // The share's rows are consecutive positions, so they need few pages:
+  // their page-table entries are copied to LDS once (when they fit).
+  auto page_index = [&](int pos) -> int {
+    return a.page_shift >= 0 ? pos >> a.page_shift : pos / a.page_size;
   };
-  auto row_ptr = [&](int r, int pg) -> const char* {
-    if (pg < 0 || pg >= a.n_pages) return nullptr;
+  const bool any_rows = seq_ok && r_hi > r_lo;
+  const int pg0 = any_rows ? page_index(start + r_lo) : 0;
+  const int n_pg = any_rows ? page_index(start + r_hi - 1) - pg0 + 1 : 0;
+  const bool cached = n_pg <= kLagPtCache;
+  int* lpt = reinterpret_cast<int*>(lds + (LAG ? lagkv_tree_floats(a.H, a.d) : 0));
+  if (cached)
+    for (int i = tid; i < n_pg; i += kLagThreads) lpt[i] = pt[pg0 + i];
+  __syncthreads();
+  // The plane's base and this lane's column: a row address is the base
+  // plus a wave-uniform row offset (row segments), to which the lane's
+  // column is added by the load itself.
+  const char* pbase = a.base + (int64_t)layer * a.s_layer + (int64_t)kv * a.s_kv;
+  const int loff = col * 16 * CPL;
+  // Byte offset (in the plane) of chunk row r, -1 if the row is not this
+  // wavefront's or its page is out of range.
+  auto row_off = [&](int r) -> int64_t {
+    if (!seq_ok || r >= s_hi) return -1;
     const int pos = start + r;
-    const int slot = a.page_shift >= 0 ? pos & (a.page_size - 1) : pos % a.page_size;
-    return plane + (int64_t)pg * a.s_page + (int64_t)slot * row_bytes + col * 16;
+    const int pidx = page_index(pos);
+    const int pg = cached ? lpt[pidx - pg0] : pt[pidx];
+    if (pg < 0 || pg >= a.n_pages) return -1;
+    return (int64_t)pg * a.s_page + (int64_t)(pos - pidx * a.page_size) * row_bytes;
   };
-
-  float mn[8], mx[8], cmn[8], cmx[8];
+  // Row segments: lane i keeps the offset of row tb + i of the wavefront's
+  // block (a table refilled every 64 rows), and a row's offset is read
+  // from it with readlane -- no memory round trip per row, and (the table
+  // being computed, not loaded) no wait for the rows in flight.
+  int tb = -(1 << 30);
+  uint32_t t_lo = 0, t_hi = 0;
+  auto row_addr = [&](int r, bool& ok) -> const char* {
+    int64_t off;
+    if (WIDE) {
+      if (r - tb >= 64 || r < tb) {
+        tb = r;
+        const int64_t o = row_off(r + lane);
+        t_lo = (uint32_t)o;
+        t_hi = (uint32_t)((uint64_t)o >> 32);
+      }
+      const uint32_t lo = __builtin_amdgcn_readlane(t_lo, r - tb);
+      const uint32_t hi = __builtin_amdgcn_readlane(t_hi, r - tb);
+      off = (int64_t)(((uint64_t)hi << 32) | lo);
+    } else {
+      off = row_off(r);
+    }
+    ok = off >= 0;
+    return ok ? pbase + off : pbase;
+  };
+  // Load the rows of sweeps it0 .. it0 + kLagAhead - 1; ok[u]: row present.
+  // Every load is issued (a missing row reads the plane's first row and is
+  // ignored), so the loads are straight-line code and the compiler can
+  // wait for each batch alone rather than for every load in flight.
+  auto load_rows = [&](int it0, u32x4 (&raw)[AH][CPL], bool (&ok)[AH]) {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+    for (int u = 0; u < AH; ++u) {
+      const char* q = row_addr(row_of(it0 + u), ok[u]);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        raw[u][c] = WIDE ? ld_row_nt(q, (uint32_t)(loff + 16 * c), row_bytes)
+                         : ld_stream(q + loff + 16 * c);
+    }
+  };
+
+  float cmn[NCH], cmx[NCH];  // this lane's channels' range over its rows
+#pragma unroll
+  for (int e = 0; e < NCH; ++e) {
     cmn[e] = __builtin_huge_valf();
     cmx[e] = -__builtin_huge_valf();
   }
-
-  // Combine the per-thread ranges of the rpp threads sharing a column.
-  auto combine = [&]() {
-    if (ro < rpp) {
+  auto unpack = [](const u32x4 (&w)[CPL], float (&x)[NCH]) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        cmb[(ro * 8 + e) * row_vec + col] = cmn[e];
-        cmb[((rpp + ro) * 8 + e) * row_vec + col] = cmx[e];
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[c * 8 + 2 * k] = bf16_lo(w[c][k]);
+        x[c * 8 + 2 * k + 1] = bf16_hi(w[c][k]);
+      }
+  };
+  auto track = [&](const float (&x)[NCH]) {
+#pragma unroll
+    for (int e = 0; e < NCH; ++e) {
+      cmn[e] = nan_min(cmn[e], x[e]);
+      cmx[e] = nan_max(cmx[e], x[e]);
+    }
+  };
+  // Combine the range over the workgroup's row slots (and the rows of one
+  // wavefront) in a fixed tree through LDS, slots of [2][H*d] floats; the
+  // partial of slot 0 ends with the result.  With `bcast` every lane then
+  // reads it.
+  const int n_part = slots * rpw;
+  const int vid = slot * rpw + rw;
+  auto combine = [&](bool bcast) {
+    for (int s = n_part / 2; s >= 1; s >>= 1) {
+      if (vid >= s && vid < 2 * s) {
+        float* sl = lds + (int64_t)(vid - s) * 2 * HD + col * NCH;
+#pragma unroll
+        for (int e = 0; e < NCH; ++e) {
+          sl[e] = cmn[e];
+          sl[HD + e] = cmx[e];
+        }
+      }
+      __syncthreads();
+      if (vid < s) {
+        const float* sl = lds + (int64_t)vid * 2 * HD + col * NCH;
+#pragma unroll
+        for (int e = 0; e < NCH; ++e) {
+          cmn[e] = nan_min(cmn[e], sl[e]);
+          cmx[e] = nan_max(cmx[e], sl[HD + e]);
+        }
+      }
+      __syncthreads();
+    }
+    if (bcast) {
+      if (vid == 0) {
+#pragma unroll
+        for (int e = 0; e < NCH; ++e) {
+          lds[col * NCH + e] = cmn[e];
+          lds[HD + col * NCH + e] = cmx[e];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < NCH; ++e) {
+        cmn[e] = lds[col * NCH + e];
+        cmx[e] = lds[HD + col * NCH + e];
       }
     }
-    __syncthreads();
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float lo = cmb[e * row_vec + col], hi = cmb[(rpp * 8 + e) * row_vec + col];
-      for (int q = 1; q < rpp; ++q) {
-        lo = nan_min(lo, cmb[(q * 8 + e) * row_vec + col]);
-        hi = nan_max(hi, cmb[((rpp + q) * 8 + e) * row_vec + col]);
-      }
-      cmn[e] = lo;
-      cmx[e] = hi;
-    }
-    __syncthreads();
   };
 
-  if (fresh) {
-    for (int r0 = r_lo + ro; r0 < r_hi && ro < rpp; r0 += kLagRowsAhead * rpp) {
-      u32x4 raw[kLagRowsAhead];
-      bool got[kLagRowsAhead];
-      int pg[kLagRowsAhead];
+  // y = (x - mn) * sc - 1/2: the normalisation (shifted by -1/2) of each
+  // channel.  The difference comes first: folding mn * sc into the
+  // addend would round at the magnitude of x * sc, which a narrow range
+  // (sc up to 1/eps) makes large.
+  float mnv[LAG ? NCH : 1], sc[LAG ? NCH : 1];
+  if (LAG) {
+    if (fresh) {
+      // first pass: the chunk's own range
+      for (int it0 = 0; it0 < sweeps; it0 += AH) {
+        u32x4 raw[AH][CPL];
+        bool ok[AH];
+        load_rows(it0, raw, ok);
 #pragma unroll
-      for (int u = 0; u < kLagRowsAhead; ++u) pg[u] = row_page(r0 + u * rpp);
-#pragma unroll
-      for (int u = 0; u < kLagRowsAhead; ++u) {
-        const char* p = row_ptr(r0 + u * rpp, pg[u]);
-        got[u] = p != nullptr;
-        if (got[u]) raw[u] = ld_stream(p);
-      }
-#pragma unroll
-      for (int u = 0; u < kLagRowsAhead; ++u) {
-        if (!got[u]) continue;
-        float x[8];
-        unpack8(raw[u], x);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          cmn[e] = nan_min(cmn[e], x[e]);
-          cmx[e] = nan_max(cmx[e], x[e]);
+        for (int u = 0; u < AH; ++u) {
+          float x[NCH];
+          unpack(raw[u], x);
+          if (ok[u]) track(x);
         }
       }
+      combine(true);
     }
-    combine();
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      mn[e] = cmn[e];
-      mx[e] = cmx[e];
-    }
-  } else if (LAG) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      mn[e] = a.range_in[rbase + e];
-      mx[e] = a.range_in[half + rbase + e];
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      mn[e] = 0.f;
-      mx[e] = 0.f;
+    for (int e = 0; e < NCH; ++e) {
+      const float mn = fresh ? cmn[e] : a.range_in[rbase + e];
+      const float mx = fresh ? cmx[e] : a.range_in[half + rbase + e];
+      mnv[e] = mn;
+      sc[e] = 1.0f / (mx - mn + a.eps);
     }
   }
-  float den[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) den[e] = 1.0f / (mx[e] - mn[e] + a.eps);
 
   const float inv_d = 1.0f / (float)a.d;
-  // All threads run the same trip count so that the head-group shuffles see
-  // every lane of the group.
-  // kLagRowsAhead rows per thread are loaded before any is used, so each
-  // thread has that many 16-byte loads in flight.
-  const int trips = (r_hi - r_lo + rpp - 1) / rpp;
-  for (int it0 = 0; it0 < trips; it0 += kLagRowsAhead) {
-    u32x4 raw[kLagRowsAhead];
-    bool got[kLagRowsAhead];
-    int pg[kLagRowsAhead];
+  const bf16x2 one2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1, 1)
+  // Variance of this lane's head for one row from the sum and the sum of
+  // squares of its values (lag-normalised: y = (x - mn) * sc - 1/2 per
+  // channel, the variance being that of x~): every lane of the wavefront runs it (the group sums see every
+  // lane of a group).  The row is always consumed and a missing one masked
+  // afterwards: a load whose value might go unused forces a wait for every
+  // load in flight before its register is reused.
+  auto finish_var = [&](float s, float q, bool ok) -> float {
+    s = group_sum(ok ? s : 0.f, gw);
+    q = group_sum(ok ? q : 0.f, gw);
+    const float mu = s * inv_d;
+    return fmaf(-mu, mu, q * inv_d);
+  };
+  // raw: x0 + x1 and x0^2 + x1^2 of each packed pair in one instruction
+  auto var_raw = [&](const u32x4 (&w)[CPL], bool ok) -> float {
+    float s = 0.f, q = 0.f;
 #pragma unroll
-    for (int u = 0; u < kLagRowsAhead; ++u) {
-      const int r = r_lo + (it0 + u) * rpp + ro;
-      pg[u] = ro < rpp ? row_page(r) : -1;
-    }
+    for (int c = 0; c < CPL; ++c)
 #pragma unroll
-    for (int u = 0; u < kLagRowsAhead; ++u) {
-      const char* p = row_ptr(r_lo + (it0 + u) * rpp + ro, pg[u]);
-      got[u] = p != nullptr;
-      if (got[u]) raw[u] = ld_stream(p);
-    }
+      for (int k = 0; k < 4; ++k) {
+        // (through a scalar: a bit cast of the vector element itself
+        // reads element 0)
+        const uint32_t wk = w[c][k];
+        const bf16x2 x = __builtin_bit_cast(bf16x2, wk);
+        s = __builtin_amdgcn_fdot2_f32_bf16(x, one2, s, false);
+        q = __builtin_amdgcn_fdot2_f32_bf16(x, x, q, false);
+      }
+    return finish_var(s, q, ok);
+  };
+
+  const bool track_range = LAG && !fresh;
+  // Rows of sweeps it0 .. it0 + kLagAhead - 1: the range, then each head's
+  // variance, written by the head's first lane (rows past the share are
+  // not written).
+  auto process = [&](int it0, const u32x4 (&raw)[AH][CPL], const bool (&ok)[AH]) {
+    float v[AH];
+    if (LAG) {
+      // rows in pairs, one packed word at a time: each value unpacked
+      // once, for the range and the sums
 #pragma unroll
-    for (int u = 0; u < kLagRowsAhead; ++u) {
-      const int r = r_lo + (it0 + u) * rpp + ro;
-      const bool live = ro < rpp && r < r_hi;
-      float x[8];
-      if (got[u]) {
-        unpack8(raw[u], x);
-        if (LAG) {
+      for (int u = 0; u < AH; u += 2) {
+        float sa = 0.f, qa = 0.f, sb = 0.f, qb = 0.f;
+        auto sums = [&](float xa, float xb, int e) {
+          const float ya = fmaf(xa - mnv[e], sc[e], -0.5f);
+          const float yb = fmaf(xb - mnv[e], sc[e], -0.5f);
+          sa += ya;
+          qa = fmaf(ya, ya, qa);
+          sb += yb;
+          qb = fmaf(yb, yb, qb);
+        };
+        if (track_range && WIDE && ok[u] && ok[u + 1]) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            cmn[e] = nan_min(cmn[e], x[e]);
-            cmx[e] = nan_max(cmx[e], x[e]);
-            x[e] = (x[e] - mn[e]) * den[e];
-          }
+          for (int c = 0; c < CPL; ++c)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const int e = c * 8 + 2 * k;
+              const float a0 = bf16_lo(raw[u][c][k]), a1 = bf16_hi(raw[u][c][k]);
+              const float b0 = bf16_lo(raw[u + 1][c][k]), b1 = bf16_hi(raw[u + 1][c][k]);
+              cmn[e] = nan_min(cmn[e], nan_min(a0, b0));
+              cmx[e] = nan_max(cmx[e], nan_max(a0, b0));
+              cmn[e + 1] = nan_min(cmn[e + 1], nan_min(a1, b1));
+              cmx[e + 1] = nan_max(cmx[e + 1], nan_max(a1, b1));
+              sums(a0, b0, e);
+              sums(a1, b1, e + 1);
+            }
+        } else {
+#pragma unroll
+          for (int c = 0; c < CPL; ++c)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const int e = c * 8 + 2 * k;
+              const float a0 = bf16_lo(raw[u][c][k]), a1 = bf16_hi(raw[u][c][k]);
+              const float b0 = bf16_lo(raw[u + 1][c][k]), b1 = bf16_hi(raw[u + 1][c][k]);
+              if (track_range && ok[u]) {
+                cmn[e] = nan_min(cmn[e], a0);
+                cmx[e] = nan_max(cmx[e], a0);
+                cmn[e + 1] = nan_min(cmn[e + 1], a1);
+                cmx[e + 1] = nan_max(cmx[e + 1], a1);
+              }
+              if (track_range && ok[u + 1]) {
+                cmn[e] = nan_min(cmn[e], b0);
+                cmx[e] = nan_max(cmx[e], b0);
+                cmn[e + 1] = nan_min(cmn[e + 1], b1);
+                cmx[e + 1] = nan_max(cmx[e + 1], b1);
+              }
+              sums(a0, b0, e);
+              sums(a1, b1, e + 1);
+            }
         }
+        v[u] = finish_var(sa, qa, ok[u]);
+        v[u + 1] = finish_var(sb, qb, ok[u + 1]);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < AH; ++u) v[u] = var_raw(raw[u], ok[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < AH; ++u) {
+      const int r = row_of(it0 + u);
+      // the heads of the segment summed in lane order: with row segments
+      // one lane per head group is read into a scalar, narrow rows add
+      // their groups with lane shuffles
+      float sum;
+      if (WIDE) {
+        sum = 0.f;
+        for (int g = 0; g < 64; g += gw)
+          sum += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[u]), g));
       } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = 0.f;
+        sum = v[u];
+        for (int off = gw; off < lpr; off <<= 1) sum += __shfl_xor(sum, off, 64);
       }
-      float s = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += x[e];
-      const float mu = group_sum(s, gl) * inv_d;
-      float q = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float dlt = x[e] - mu;
-        q = fmaf(dlt, dlt, q);
-      }
-      const float var = group_sum(q, gl) * inv_d;
-      if (live && (col % gl) == 0) vbuf[head * vld + r] = got[u] ? var : 0.f;
+      if (li == 0 && r < s_hi) part[r] = ok[u] ? sum : 0.f;
     }
+  };
+  // Software pipelined over two buffers: the next batch of rows is in
+  // flight while this one is used.
+  u32x4 ra[AH][CPL], rb[AH][CPL];
+  bool oa[AH], ob[AH];
+  if (sweeps > 0) load_rows(0, ra, oa);
+  for (int it0 = 0; it0 < sweeps; it0 += 2 * AH) {
+    if (it0 + AH < sweeps) load_rows(it0 + AH, rb, ob);
+    process(it0, ra, oa);
+    if (it0 + AH >= sweeps) break;
+    if (it0 + 2 * AH < sweeps) load_rows(it0 + 2 * AH, ra, oa);
+    process(it0 + AH, rb, ob);
   }
-  __syncthreads();
+
   if (LAG) {
-    // this share's range of the chunk; the reduce kernel combines the shares
-    combine();
-    if (ro == 0) {
-      float* pr = a.prange + (int64_t)sp * 2 * half;
+    if (!fresh) combine(false);
+    if (vid == 0) {
+      // the chunk's range: straight into the state when one workgroup saw
+      // every row, else this share's part for the second kernel
+      float* dst = a.splits == 1 ? a.range_out : a.prange + (int64_t)sp * 2 * half;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pr[rbase + e] = cmn[e];
-        pr[half + rbase + e] = cmx[e];
+      for (int e = 0; e < NCH; ++e) {
+        dst[rbase + e] = cmn[e];
+        dst[half + rbase + e] = cmx[e];
+      }
+      if (a.splits == 1 && !a.two) {
+        // a one-tensor signal carries no range for the other tensor
+        const int64_t other = rbase + (int64_t)(1 - 2 * kv) * HD;
+#pragma unroll
+        for (int e = 0; e < NCH; ++e) {
+          a.range_out[other + e] = 0.f;
+          a.range_out[half + other + e] = 0.f;
+        }
       }
     }
-  }
-  for (int r = r_lo + tid; r < r_hi; r += kScoreThreads) {
-    float s = 0.f;
-    for (int h = 0; h < a.H; ++h) s += vbuf[h * vld + r];
-    part[r] = s;
   }
 }
 
-// Blocks [0, tok_blocks) of each sequence: q(t) = the 2L plane sums of
-// token t in a fixed order, times 1/(L*H).  The remaining blocks (lag
-// signals): each channel's range over the chunk = the min and max of the
-// shares' partial ranges, in a fixed order.
+// Blocks [0, tok_blocks) of each sequence: q(t) = the sum of token t's
+// partial sums over the used planes and row segments, times 1/(L*H).  A
+// block takes kRedTok tokens; its kScoreThreads / kRedTok parts each add
+// every parts-th partial in order, then the parts are added in order.  The
+// remaining blocks (split rows of a lag-normalised signal): each channel's
+// range over the chunk = the min and max of the shares' partial ranges, in
+// a fixed order.
+constexpr int kRedTok = 64;
+constexpr int kRedParts = kScoreThreads / kRedTok;
+
 __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
+  __shared__ float red[kRedParts][kRedTok];
   const int b = blockIdx.y;
-  const int tok_blocks = (a.C + kScoreThreads - 1) / kScoreThreads;
+  const int tok_blocks = (a.C + kRedTok - 1) / kRedTok;
   if ((int)blockIdx.x < tok_blocks) {
-    const int c = blockIdx.x * kScoreThreads + threadIdx.x;
-    if (c >= a.C) return;
-    const float* p = a.partial + (int64_t)b * a.n_lk * a.C + c;
+    const int t = threadIdx.x % kRedTok;
+    const int part = threadIdx.x / kRedTok;
+    const int c = blockIdx.x * kRedTok + t;
     float s = 0.f;
+    if (c < a.C) {
+      const float* p = a.partial + (int64_t)b * a.n_sums * a.C + c;
 #pragma unroll 8
-    for (int lk = 0; lk < a.n_lk; ++lk) s += p[(int64_t)lk * a.C];
-    a.sig[(int64_t)b * a.C + c] = s * a.inv_count;
+      for (int pl = part; pl < a.n_sums; pl += kRedParts) s += p[(int64_t)pl * a.C];
+    }
+    red[part][t] = s;
+    __syncthreads();
+    if (part == 0 && c < a.C) {
+      float q = red[0][t];
+#pragma unroll
+      for (int k = 1; k < kRedParts; ++k) q += red[k][t];
+      a.sig[(int64_t)b * a.C + c] = q * a.inv_count;
+    }
     return;
   }
   const int i = ((int)blockIdx.x - tok_blocks) * kScoreThreads + threadIdx.x;
   if (i >= a.n_chan) return;
   const int64_t half = (int64_t)a.B * a.n_chan;
   const int64_t o = (int64_t)b * a.n_chan + i;
-  const int kv = (i / (a.n_chan / a.n_lk)) & 1;
+  const int kv = (i / (a.n_chan / (2 * a.L))) & 1;
   float lo = 0.f, hi = 0.f;  // planes of an unused tensor carry no range
   if (kv == 0 ? a.use_k : a.use_v) {
     lo = a.prange[o];
@@ -332,30 +528,32 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
   a.range_out[half + o] = hi;
 }
 
+template <bool WIDE, int CPL>
+hipError_t launch_lag(const ScoreLagArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_planes, a.B, a.splits);
+  const size_t lds = lagkv_lds_bytes(a.H, a.d, a.lag);
+  if (CPL == 1 && a.lag)
+    hipLaunchKernelGGL((k_score_lagkv<true, WIDE, 1>), grid, dim3(kLagThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL((k_score_lagkv<false, WIDE, CPL>), grid, dim3(kLagThreads), lds, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
-size_t lagkv_lds_bytes(int C, int H, int d) {
-  const int HD = H * d;
-  const int rpp = kScoreThreads / (HD / 8);
-  return (size_t)(C + 1) * H * 4 + (size_t)2 * rpp * HD * 4;
+size_t lagkv_lds_bytes(int H, int d, bool lag) {
+  return (lag ? lagkv_tree_floats(H, d) * sizeof(float) : 0) + kLagPtCache * sizeof(int);
 }
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
-  const size_t lds = lagkv_lds_bytes(a.C, a.H, a.d);
-  const dim3 grid(2 * a.L, a.B, a.splits);
-  const bool wr = a.H * a.d / 8 >= 64;
-  if (a.lag && wr)
-    hipLaunchKernelGGL((k_score_lagkv<true, true>), grid, dim3(kScoreThreads), lds, s, a);
-  else if (a.lag)
-    hipLaunchKernelGGL((k_score_lagkv<true, false>), grid, dim3(kScoreThreads), lds, s, a);
-  else if (wr)
-    hipLaunchKernelGGL((k_score_lagkv<false, true>), grid, dim3(kScoreThreads), lds, s, a);
-  else
-    hipLaunchKernelGGL((k_score_lagkv<false, false>), grid, dim3(kScoreThreads), lds, s, a);
-  hipError_t e = hipGetLastError();
+  const int cpl = lagkv_cpl(a.H, a.d, a.lag);
+  const int row_vec = a.H * a.d / 8;
+  const hipError_t e = cpl == 2        ? launch_lag<true, 2>(a, s)
+                       : row_vec >= 64 ? launch_lag<true, 1>(a, s)
+                                       : launch_lag<false, 1>(a, s);
   if (e != hipSuccess) return e;
-  const int tok_blocks = (r.C + kScoreThreads - 1) / kScoreThreads;
-  const int rng_blocks = r.lag ? (r.n_chan + kScoreThreads - 1) / kScoreThreads : 0;
+  const int tok_blocks = (r.C + kRedTok - 1) / kRedTok;
+  const int rng_blocks = r.lag && r.splits > 1 ? (r.n_chan + kScoreThreads - 1) / kScoreThreads : 0;
   hipLaunchKernelGGL(k_lag_reduce, dim3(tok_blocks + rng_blocks, r.B), dim3(kScoreThreads), 0, s,
                      r);
   return hipGetLastError();

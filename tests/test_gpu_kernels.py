@@ -322,6 +322,16 @@ def test_kv_signals_match_oracle(E, signal, C):
     _run_kv(E, signal, C)
 
 
+@pytest.mark.parametrize("H,d", [(1, 64), (2, 128), (4, 128), (2, 256),
+                                 (16, 128), (8, 256)])
+@pytest.mark.parametrize("signal", ["lagkv", "kv_val", "lagkv_key"])
+def test_kv_signals_head_shapes(E, signal, H, d):
+    """Rows of 64 to 2048 channels: several narrow rows per wavefront
+    (64, 256 channels), one wavefront per row (512) and rows split into 2
+    or 4 wavefront segments (1024, 2048), heads of 64 to 256 channels."""
+    _run_kv(E, signal, 37, H=H, d=d)
+
+
 @pytest.mark.parametrize("signal", ["lagkv", "kv_key"])
 def test_kv_signal_nan_propagates_as_in_the_oracle(E, signal):
     """A NaN key channel of one token: its variance is NaN, the trailing
@@ -331,21 +341,22 @@ def test_kv_signal_nan_propagates_as_in_the_oracle(E, signal):
     _run_kv(E, signal, 64, nan=True)
 
 
-def _run_kv(E, signal, C, nan=False):
+def _run_kv(E, signal, C, nan=False, H=8, d=128):
     import torch
-    print(f"kv signal {signal} C={C} nan={nan}", flush=True)
+    print(f"kv signal {signal} C={C} nan={nan} H={H} d={d}", flush=True)
     use_k, use_v, lag = KV_SIGNALS[signal]
     sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
               "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
     g = synth.rng(500)
-    L, H, d, page, B, w = 4, 8, 128, 16, 2, 64
+    L, page, B, w = 4, 16, 2, 64
     n_chunks = 3
     T = C * n_chunks
     Ns = np.array([T, T + 16])       # seq 1 has 16 older tokens first
     pt, n_pages = synth.page_tables(Ns, page, g)
     pool = np.zeros((L, 2, n_pages, page, H * d), dtype=np.uint16)
     tok = []   # logical rows per sequence [N][L][2][H*d]
-    wl = synth.workload("lagkv_batch8", B=B, n_layers=L)
+    wl = synth.workload("lagkv_batch8", B=B, n_layers=L, n_kv_heads=H,
+                        head_dim=d)
     for b in range(B):
         chunks = [synth.kv_rows(g, (C, L, 2, H, d),
                                 synth.lagkv_channel_scale(wl, g, j))
@@ -359,8 +370,8 @@ def _run_kv(E, signal, C, nan=False):
         tok.append(rows)
         pos = np.arange(Ns[b])
         pool[:, :, pt[b, pos // page], pos % page] = rows.transpose(1, 2, 0, 3)
-    cfg = E.default_cfg(batch=B, n_layers=L, signal=sig_id,
-                        smoothing=E.SMOOTH_MEAN, budget=4096)
+    cfg = E.default_cfg(batch=B, n_layers=L, n_kv_heads=H, head_dim=d,
+                        signal=sig_id, smoothing=E.SMOOTH_MEAN, budget=4096)
     st = [torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
           for _ in range(2)]
     E.epikv_state_init(cfg, st[0])
