@@ -439,7 +439,9 @@ def whole_pages(keep, n_keep, page):
 
 def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
                         scores, dscores, ld_s, status, cws, reps):
-    """Time epikv_compact and epikv_compact_inplace on the same kept sets.
+    """Time epikv_compact (into contiguous and into randomly placed
+    destination pages), epikv_compact_inplace and epikv_compact_remap on the
+    same kept sets.
     The in-place call rewrites the source pool: its later repetitions move
     the same slots (the cost depends on the kept sets, not the bytes)."""
     kh, nk = keep.cpu().numpy(), n_keep.cpu().numpy()
@@ -451,6 +453,16 @@ def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
         cfg, src, src_pt, src_pt.shape[1], dst, dst_pt, dst_pt.shape[1],
         keep, n_keep, scores, dscores, None, None, ld_s, status, cws,
         cws.numel()), reps)
+    # the same rebuild into the same destination pages placed at random
+    # (the fragmented pool of a long-running allocator)
+    import torch
+    perm = torch.from_numpy(synth.rng(w.seed + 13).permutation(
+        int(dst.n_pages)).astype(np.int32)).to(dst_pt.device)
+    dst_pt_scat = perm[dst_pt.long()].contiguous()
+    ms_scat = _time_calls(lambda: E.epikv_compact(
+        cfg, src, src_pt, src_pt.shape[1], dst, dst_pt_scat,
+        dst_pt_scat.shape[1], keep, n_keep, scores, dscores, None, None,
+        ld_s, status, cws, cws.numel()), reps)
     ms_in = _time_calls(lambda: E.epikv_compact_inplace(
         cfg, src, src_pt, src_pt.shape[1], keep, n_keep, scores, None, ld_s,
         status, cws, cws.numel()), reps)
@@ -466,9 +478,12 @@ def compare_compactions(E, cfg, w, src, src_pt, dst, dst_pt, keep, n_keep,
     in_bytes = moved * (2 * row + 8)
     return {"rows_kept": kept, "rows_moved_in_place": moved,
             "pages_remapped": pages, "rows_moved_remap": moved_remap,
-            "ms_out_of_place": round(ms_out, 4), "ms_in_place": round(ms_in, 4),
+            "ms_out_of_place": round(ms_out, 4),
+            "ms_out_of_place_scattered_pages": round(ms_scat, 4),
+            "ms_in_place": round(ms_in, 4),
             "ms_remap": round(ms_remap, 4),
             "gbps_out_of_place": round(out_bytes / ms_out / 1e6, 1),
+            "gbps_out_of_place_scattered_pages": round(out_bytes / ms_scat / 1e6, 1),
             "gbps_in_place": round(in_bytes / ms_in / 1e6, 1),
             "gbps_remap": round(moved_remap * (2 * row) / ms_remap / 1e6, 1)}
 

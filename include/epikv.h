@@ -188,10 +188,10 @@ int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
 
 /* Device scratch of epikv_compact, epikv_compact_inplace and
- * epikv_compact_remap: 16 bytes per (sequence, kept slot), B*K*16 rounded up
- * to 256, then 8 bytes per sequence rounded up to 256, then 16 bytes per
- * (sequence, page of the budget), B*ceil(K/page_size)*16 rounded up to 256.
- * 0 for an invalid cfg. */
+ * epikv_compact_remap: 16 bytes per slot of each sequence's budget pages,
+ * B*ceil(K/page_size)*page_size*16 rounded up to 256, then 8 bytes per
+ * sequence rounded up to 256, then 16 bytes per (sequence, page of the
+ * budget), B*ceil(K/page_size)*16 rounded up to 256.  0 for an invalid cfg. */
 size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg);
 
 /* Reset a state buffer of epikv_state_bytes(cfg) bytes to the start of a

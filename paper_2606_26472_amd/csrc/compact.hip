@@ -4,64 +4,220 @@
 // (layer, K|V) holds all KV heads (n_kv_heads * head_dim bf16, 2 KiB for
 // 8 x 128), so the copy is a gather of 2 KiB rows: pure HBM streaming.
 //
-// Two kernels:
-//   resolve  one thread per kept slot turns keep_idx and the two page tables
-//            into the byte offsets of the source and destination rows inside
-//            a plane (one 16-byte record per slot, in the workspace), and
-//            copies the slot's score and position;
-//   gather   a 256-thread workgroup owns four consecutive slots of one
-//            sequence (one wavefront per slot) for lk_per_block planes.  The
-//            wavefront reads its slot's offset record with a scalar load and
-//            then streams the row's 16-byte columns of every plane: a single
-//            dependent load before the data, so short-lived workgroups keep
-//            HBM busy.  Loads and stores are non-temporal: each byte is
-//            touched once.  The hardware deals workgroups to the 8 XCDs
-//            round-robin; the gather remaps its block index so that each XCD
-//            streams one contiguous range of destination slots (measured
-//            2-4% faster than the interleaved order).  The gather reserves
-//            LDS it does not use so that at most six workgroups (24
-//            wavefronts) share a CU: fewer requests in flight keep HBM more
-//            efficient here (measured 2% faster than eight per CU, and
-//            faster than five or seven).
+// Three kernels:
+//   order    one workgroup ranks every (sequence, destination page) by its
+//            page id, i.e. by physical address: the used pages first, in
+//            ascending page id, then the unused ones.  Writing the rebuilt
+//            cache in that order streams the writes through memory the way
+//            a plain copy does even when the allocator scattered the
+//            destination pages (measured on MI355X: 5.2 -> 6.2 TB/s for
+//            randomly placed pages; a cache rebuilt into one run of pages
+//            per sequence is already in that order).  Page ids of the used
+//            pages are marked in an LDS bitmap over their range, and a page's
+//            rank is the number of marked ids below it.  A range too wide
+//            for the bitmap, or a page id used twice, keeps the logical
+//            order (sequence, page).
+//   resolve  one thread per slot of the budget's pages turns keep_idx and
+//            the two page tables into the byte offsets of the source and
+//            destination rows inside a plane, a 16-byte record written at
+//            position rank(sequence, page) * page_size + slot (slots past
+//            n_keep, and rows out of range, get an empty record), and copies
+//            the slot's score and position;
+//   gather   a 64-thread workgroup copies 64 16-byte columns (1 KiB: half a
+//            2 KiB row) of one record in one (layer, K|V) plane: it reads the
+//            record with a scalar load and streams the columns, one load
+//            and one store per lane, non-temporal (each byte is touched
+//            once).  Workgroups walk the records in order, so consecutive
+//            workgroups write consecutive addresses.  (Measured on the
+//            32 x 4096-row rebuild: 1 KiB workgroups 2% faster than four
+//            2 KiB rows per 256-thread workgroup.)
 #include "epikv_internal.h"
 
 namespace epikv {
 namespace {
 
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderWords = 16384;  // bitmap words: page ids spanning up to 512 Ki
+
+__global__ __launch_bounds__(kOrderThreads) void k_compact_order(CompactArgs a) {
+  __shared__ uint32_t bits[kOrderWords];
+  __shared__ uint32_t pre[kOrderThreads];  // per-thread prefix (bitmap chunks, then invalid entries)
+  __shared__ uint32_t wsum[kOrderThreads / 64];
+  __shared__ int s_lo, s_hi, s_logical;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int n_pg = a.n_pg;
+  const int64_t N = (int64_t)a.B * n_pg;
+  int32_t* rank = a.rank;
+
+  // Destination page of entry e = b * n_pg + m, or -1 if the page is not
+  // used (past n_keep, a refused sequence) or out of range.
+  auto page_of = [&](int64_t e) -> int {
+    const int b = (int)(e / n_pg);
+    const int m = (int)(e - (int64_t)b * n_pg);
+    const int nk = min(a.n_keep[b], a.K);
+    if (nk <= 0 || (int64_t)m * a.page_size >= nk || m >= a.ld_dst_pt) return -1;
+    const int pg = a.dst_pt[(int64_t)b * a.ld_dst_pt + m];
+    return (pg >= 0 && pg < a.d_npages) ? pg : -1;
+  };
+
+  // 1. the range of the used page ids
+  int lo = INT32_MAX, hi = -1;
+  for (int64_t e = tid; e < N; e += kOrderThreads) {
+    const int pg = page_of(e);
+    if (pg >= 0) {
+      lo = min(lo, pg);
+      hi = max(hi, pg);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = min(lo, __shfl_xor(lo, off, 64));
+    hi = max(hi, __shfl_xor(hi, off, 64));
+  }
+  if (tid == 0) {
+    s_lo = INT32_MAX;
+    s_hi = -1;
+    s_logical = 0;
+  }
+  __syncthreads();
+  if (lane == 0) {
+    atomicMin(&s_lo, lo);
+    atomicMax(&s_hi, hi);
+  }
+  __syncthreads();
+  lo = s_lo;
+  hi = s_hi;
+  const int64_t span = hi >= lo ? (int64_t)hi - lo + 1 : 0;
+  const int words = (int)((span + 31) / 32);
+  bool logical = span == 0 || words > kOrderWords;
+
+  // 2. mark the used page ids (a page used twice keeps the logical order)
+  if (!logical) {
+    for (int w = tid; w < words; w += kOrderThreads) bits[w] = 0u;
+    __syncthreads();
+    for (int64_t e = tid; e < N; e += kOrderThreads) {
+      const int pg = page_of(e);
+      if (pg >= 0) {
+        const uint32_t bit = 1u << ((pg - lo) & 31);
+        if (atomicOr(&bits[(pg - lo) >> 5], bit) & bit) s_logical = 1;
+      }
+    }
+    __syncthreads();
+    logical = s_logical != 0;
+  }
+
+  // 3. ranks: a used page's is the number of used ids below it; the
+  //    unused entries follow, in logical order
+  const int chunk = (words + kOrderThreads - 1) / kOrderThreads;  // bitmap words per thread
+  uint32_t n_used = 0;
+  if (!logical) {
+    uint32_t c = 0;
+    for (int k = 0; k < chunk; ++k) {
+      const int w = tid * chunk + k;
+      if (w < words) c += __popc(bits[w]);
+    }
+    // exclusive scan of the per-thread counts
+    uint32_t x = c;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t t = __shfl_up(x, off, 64);
+      if (lane >= off) x += t;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    uint32_t base = 0, tot = 0;
+    for (int w = 0; w < kOrderThreads / 64; ++w) {
+      base += w < wave ? wsum[w] : 0u;
+      tot += wsum[w];
+    }
+    pre[tid] = base + x - c;
+    n_used = tot;
+    __syncthreads();
+  }
+  // invalid entries, counted in contiguous per-thread ranges of entries
+  const int64_t per = (N + kOrderThreads - 1) / kOrderThreads;
+  const int64_t e0 = (int64_t)tid * per;
+  uint32_t n_bad = 0;
+  if (!logical)
+    for (int64_t e = e0; e < min(N, e0 + per); ++e) n_bad += page_of(e) < 0 ? 1u : 0u;
+  uint32_t bad_before = 0;
+  {
+    uint32_t x = n_bad;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t t = __shfl_up(x, off, 64);
+      if (lane >= off) x += t;
+    }
+    __syncthreads();  // (wsum is reused)
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+    bad_before = base + x - n_bad;
+  }
+  for (int64_t e = e0; e < min(N, e0 + per); ++e) {
+    int32_t r;
+    if (logical) {
+      r = (int32_t)e;
+    } else {
+      const int pg = page_of(e);
+      if (pg >= 0) {
+        const int i = pg - lo;
+        const int w = i >> 5;
+        const int owner = w / chunk;
+        uint32_t below = pre[owner];
+        for (int k = owner * chunk; k < w; ++k) below += __popc(bits[k]);
+        below += __popc(bits[w] & ((1u << (i & 31)) - 1u));
+        r = (int32_t)below;
+      } else {
+        r = (int32_t)(n_used + bad_before++);
+      }
+    }
+    rank[e] = r;
+  }
+}
+
 __global__ __launch_bounds__(kCompactThreads) void k_compact_resolve(CompactArgs a) {
   const int j = blockIdx.x * kCompactThreads + threadIdx.x;
   const int b = blockIdx.y;
+  const int slots = a.n_pg * a.page_size;  // slots of the budget's pages
+  if (j >= slots) return;
+  const int m = j / a.page_size;
+  const int slot_in = j - m * a.page_size;
   // A caller's n_keep above K is clamped so keep_idx is never read past the
-  // sequence's row.
+  // sequence's row; n_keep < 0: sequence untouched.
   const int nk = min(a.n_keep[b], a.K);
-  if (j >= nk) return;  // also n_keep < 0: sequence untouched
-  const int idx = a.keep_idx[(int64_t)b * a.K + j];
   int64_t so = -1, dso = -1;
-  if (idx >= 0) {
-    const int sp = idx / a.page_size;
-    const int slot = idx - sp * a.page_size;
-    if ((int64_t)sp < a.ld_src_pt) {
-      const int pg = a.src_pt[(int64_t)b * a.ld_src_pt + sp];
-      if (pg >= 0 && pg < a.s_npages) so = (int64_t)pg * a.s_page + (int64_t)slot * a.row_bytes;
+  int idx = -1;
+  bool bad = false;
+  if (j < nk) {
+    idx = a.keep_idx[(int64_t)b * a.K + j];
+    if (idx >= 0) {
+      const int sp = idx / a.page_size;
+      const int slot = idx - sp * a.page_size;
+      if ((int64_t)sp < a.ld_src_pt) {
+        const int pg = a.src_pt[(int64_t)b * a.ld_src_pt + sp];
+        if (pg >= 0 && pg < a.s_npages) so = (int64_t)pg * a.s_page + (int64_t)slot * a.row_bytes;
+      }
     }
-  }
-  {
-    const int dp = j / a.page_size;
-    const int dslot = j - dp * a.page_size;
-    if ((int64_t)dp < a.ld_dst_pt) {
-      const int pg = a.dst_pt[(int64_t)b * a.ld_dst_pt + dp];
-      if (pg >= 0 && pg < a.d_npages) dso = (int64_t)pg * a.d_page + (int64_t)dslot * a.row_bytes;
+    if ((int64_t)m < a.ld_dst_pt) {
+      const int pg = a.dst_pt[(int64_t)b * a.ld_dst_pt + m];
+      if (pg >= 0 && pg < a.d_npages) dso = (int64_t)pg * a.d_page + (int64_t)slot_in * a.row_bytes;
     }
+    bad = so < 0 || dso < 0;
   }
-  const bool ok = so >= 0 && dso >= 0;
-  int64_t* rec = a.offsets + 2 * ((int64_t)b * a.K + j);
+  const bool ok = j < nk && !bad;
+  const int64_t pos = (int64_t)a.rank[(int64_t)b * a.n_pg + m] * a.page_size + slot_in;
+  int64_t* rec = a.offsets + 2 * pos;
   rec[0] = ok ? so : -1;
   rec[1] = ok ? dso : -1;
-  if (!ok) {
+  if (bad) {
     if (a.seq_status) a.seq_status[b] = EPIKV_SEQ_RANGE;
     return;
   }
-  if ((int64_t)idx < a.ld_s && (int64_t)j < a.ld_s) {
+  if (ok && (int64_t)idx < a.ld_s && (int64_t)j < a.ld_s) {
     const int64_t si = (int64_t)b * a.ld_s + idx;
     const int64_t di = (int64_t)b * a.ld_s + j;
     if (a.dst_scores) a.dst_scores[di] = a.src_scores[si];
@@ -69,94 +225,48 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_resolve(CompactArgs
   }
 }
 
-// One wavefront per destination row: the row's offset record, n_keep and
-// the plane bases are wave-uniform (scalar loads), lane l streams the
-// row's 16-byte columns l, l+64, ... (NV of them) of each plane.
-template <int NV, int PL>
-__global__ __launch_bounds__(kCompactThreads) void k_compact(CompactArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int b = blockIdx.z;
-  // XCD-aware: hardware places block x on XCD x % 8; give each XCD a
-  // contiguous range of slot groups.
-  const int nx = gridDim.x;
-  int bx = blockIdx.x;
-  if ((nx & 7) == 0) bx = (bx & 7) * (nx >> 3) + (bx >> 3);
-  const int j = bx * kCompactWaves + wave;
-  const int row_vec = a.row_bytes >> 4;
-  // The record of slot min(j, K-1) is always readable, so it is fetched
-  // together with n_keep instead of after it.
-  const int64_t* rec = a.offsets + 2 * ((int64_t)b * a.K + min(j, a.K - 1));
+// Workgroup x (linear over blockIdx.z, blockIdx.x): record x / units, its
+// columns [64 u, 64 u + 64) with u = x % units, in plane blockIdx.y.  The
+// record is wave-uniform (a scalar load); lanes past the row's columns idle.
+__global__ __launch_bounds__(64) void k_compact(CompactArgs a, int64_t total) {
+  const int lane = threadIdx.x;
+  const int64_t x = (int64_t)blockIdx.z * gridDim.x + blockIdx.x;
+  if (x >= total) return;
+  const int64_t r = x / a.units;
+  const int u = (int)(x - r * a.units);
+  const int64_t* rec = a.offsets + 2 * r;
   const int64_t s0 = rec[0];
   const int64_t d0 = rec[1];
-  const int nk = min(a.n_keep[b], a.K);
-  if (j >= nk || s0 < 0) return;
-
-  const int lk0 = blockIdx.y * a.lk_per_block;
-  const int lk1 = min(a.n_lk, lk0 + a.lk_per_block);
-  for (int lk = lk0; lk < lk1; lk += PL) {
-    u32x4 val[PL][NV];
-#pragma unroll
-    for (int p = 0; p < PL; ++p) {
-      const int pl = lk + p;
-      if (pl < lk1) {
-        const char* sb = a.src + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + s0;
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-          const int c = lane + q * 64;
-          if (c < row_vec) val[p][q] = ld_stream(sb + (int64_t)c * 16);
-        }
-      }
-    }
-#pragma unroll
-    for (int p = 0; p < PL; ++p) {
-      const int pl = lk + p;
-      if (pl < lk1) {
-        char* db = a.dst + (int64_t)(pl >> 1) * a.d_layer + (int64_t)(pl & 1) * a.d_kv + d0;
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-          const int c = lane + q * 64;
-          if (c < row_vec) st_stream(db + (int64_t)c * 16, val[p][q]);
-        }
-      }
-    }
-  }
-}
-
-template <int NV, int PL>
-hipError_t launch(const CompactArgs& a, hipStream_t s) {
-  dim3 grid(a.blocks_per_seq, (a.n_lk + a.lk_per_block - 1) / a.lk_per_block, a.B);
-  hipLaunchKernelGGL((k_compact<NV, PL>), grid, dim3(kCompactThreads), kCompactLdsCap, s, a);
-  return hipGetLastError();
-}
-
-template <int PL>
-hipError_t launch_nv(const CompactArgs& a, hipStream_t s) {
-  const int row_vec = a.row_bytes >> 4;
-  if (row_vec <= 64) return launch<1, PL>(a, s);
-  if (row_vec <= 128) return launch<2, PL>(a, s);
-  if (row_vec <= 256) return launch<4, PL>(a, s);
-  return hipErrorInvalidValue;
+  if (s0 < 0) return;
+  const int c = u * 64 + lane;
+  if (c >= (a.row_bytes >> 4)) return;
+  const int pl = blockIdx.y;
+  const char* sb = a.src + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + s0;
+  char* db = a.dst + (int64_t)(pl >> 1) * a.d_layer + (int64_t)(pl & 1) * a.d_kv + d0;
+  st_stream(db + (int64_t)c * 16, ld_stream(sb + (int64_t)c * 16));
 }
 
 }  // namespace
 
 hipError_t launch_compact(const CompactArgs& args, hipStream_t s) {
   CompactArgs a = args;
-  // One wavefront per destination row, four rows and one (layer, K|V) plane
-  // per workgroup: measured best on MI355X among 2..16 rows x 1..64 planes
-  // for 32 sequences keeping 4096 of 8k..32k tokens.  (A wavefront here has
-  // one 1 KiB load in flight at a time -- the compiler waits between the
-  // guarded loads; a branch-free variant with both loads in flight measured
-  // 5% slower at eight workgroups per CU, and more planes per wavefront
-  // slower still.)
-  a.lk_per_block = 1;
-  a.blocks_per_seq = (a.K + kCompactWaves - 1) / kCompactWaves;
-  hipLaunchKernelGGL(k_compact_resolve, dim3((a.K + kCompactThreads - 1) / kCompactThreads, a.B),
-                     dim3(kCompactThreads), 0, s, a);
-  const hipError_t e = hipGetLastError();
+  a.units = ((a.row_bytes >> 4) + 63) / 64;
+  hipLaunchKernelGGL(k_compact_order, dim3(1), dim3(kOrderThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_nv<1>(a, s);
+  const int slots = a.n_pg * a.page_size;
+  hipLaunchKernelGGL(k_compact_resolve, dim3((slots + kCompactThreads - 1) / kCompactThreads, a.B),
+                     dim3(kCompactThreads), 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // workgroups (record, column group) in order, the linear index split as
+  // blockIdx.z * gridDim.x + blockIdx.x
+  const int64_t total = (int64_t)a.B * slots * a.units;
+  const int64_t gx = total < kCompactGridX ? total : kCompactGridX;
+  const int64_t gz = (total + gx - 1) / gx;
+  hipLaunchKernelGGL(k_compact, dim3((unsigned)gx, a.n_lk, (unsigned)gz), dim3(64), 0, s, a,
+                     total);
+  return hipGetLastError();
 }
 
 }  // namespace epikv

@@ -70,14 +70,17 @@ size_t sig_bytes(const epikv_cfg* c, int chunk) {
   return align_up(4 * (size_t)n_sig(c) * (size_t)c->batch * (size_t)chunk);
 }
 
-// Row offset records [B][K][2] int64, then (in place) [B][2] int32, then
-// (page remapping) [B][4][ceil(K / page_size)] int32.
-size_t compact_records_bytes(const epikv_cfg* c) {
-  return align_up(16 * (size_t)c->batch * (size_t)c->budget);
-}
-
 int budget_pages(const epikv_cfg* c) {
   return (int)(((int64_t)c->budget + c->page_size - 1) / c->page_size);
+}
+
+// Row offset records, 16 bytes per slot of the budget's pages (out of
+// place: in destination-page rank order; in place: [B][K]), then (in place)
+// [B][2] int32, then [B][4][ceil(K / page_size)] int32 (page remapping;
+// out of place, the first [B][ceil(K / page_size)] hold the destination
+// pages' ranks).
+size_t compact_records_bytes(const epikv_cfg* c) {
+  return align_up(16 * (size_t)c->batch * (size_t)budget_pages(c) * (size_t)c->page_size);
 }
 
 size_t compact_ws_bytes(const epikv_cfg* c) {
@@ -471,11 +474,14 @@ CompactArgs compact_args(const epikv_cfg* c, const epikv_pool* src, const int32_
   a.ld_s = ld_s;
   a.seq_status = seq_status;
   a.offsets = (int64_t*)ws;
+  a.rank = (int32_t*)((char*)ws + compact_records_bytes(c) + align_up(8 * (size_t)c->batch));
   a.B = c->batch;
   a.K = c->budget;
   a.page_size = c->page_size;
   a.row_bytes = row_bytes(c);
   a.n_lk = 2 * c->n_layers;
+  a.n_pg = budget_pages(c);
+  a.units = 0;
   return a;
 }
 

@@ -143,11 +143,12 @@ struct CompactArgs {
   int32_t* dst_pos;
   int64_t ld_s;
   int32_t* seq_status;                     // optional
-  int64_t* offsets;                        // workspace [B][K][2]: src, dst byte offsets
+  int64_t* offsets;                        // workspace [B * n_pg * page_size][2]: src, dst
+                                           // byte offsets, in destination-page rank order
+  int32_t* rank;                           // workspace [B][n_pg]: rank of each destination page
   int32_t B, K, page_size, row_bytes, n_lk;
-  // launch shape, chosen by launch_compact
-  int32_t lk_per_block;                    // (layer, K|V) planes per workgroup
-  int32_t blocks_per_seq;                  // ceil(K / kCompactWaves)
+  int32_t n_pg;                            // pages of the budget: ceil(K / page_size)
+  int32_t units;                           // 1 KiB column groups per row (set by launch_compact)
 };
 
 struct InplaceArgs {
@@ -280,11 +281,9 @@ constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
 constexpr int kTokMaxRow = 4096;         // fused per-token scorer: widest hidden row
 constexpr int kSelectThreads = 1024;
-constexpr int kCompactThreads = 256;
-constexpr int kCompactWaves = kCompactThreads / 64;  // destination slots per gather workgroup
-// Dynamic LDS the gather reserves (and never touches) to cap it at six
-// workgroups per CU: 160 KiB of LDS per CU on gfx950 / 24 KiB = 6.
-constexpr int kCompactLdsCap = 24 * 1024;
+constexpr int kCompactThreads = 256;      // resolve kernel; in-place move workgroups
+constexpr int64_t kCompactGridX = 1 << 24;  // gather workgroups per grid row
+constexpr int kCompactWaves = kCompactThreads / 64;  // walks per in-place move workgroup
 constexpr int kLagWaves = 8;             // wavefronts per KV-vector scorer workgroup
 constexpr int kLagThreads = kLagWaves * 64;
 constexpr int kLagAhead = 4;             // rows a KV-scorer wavefront loads before using them (even)
