@@ -329,17 +329,17 @@ void k_score_lagkv(ScoreLagArgs a) {
   // Variance of this lane's head for one row from the sum and the sum of
   // squares of its values (lag-normalised: y = (x - mn) * sc - 1/2 per
   // channel, the variance being that of x~): every lane of the wavefront runs it (the group sums see every
-  // lane of a group).  The row is always consumed and a missing one masked
-  // afterwards: a load whose value might go unused forces a wait for every
-  // load in flight before its register is reused.
-  auto finish_var = [&](float s, float q, bool ok) -> float {
-    s = group_sum(ok ? s : 0.f, gw);
-    q = group_sum(ok ? q : 0.f, gw);
+  // lane of a group).  A missing row is computed like any other and its
+  // result dropped at the write: a load whose value might go unused forces
+  // a wait for every load in flight before its register is reused.
+  auto finish_var = [&](float s, float q) -> float {
+    s = group_sum(s, gw);
+    q = group_sum(q, gw);
     const float mu = s * inv_d;
     return fmaf(-mu, mu, q * inv_d);
   };
   // raw: x0 + x1 and x0^2 + x1^2 of each packed pair in one instruction
-  auto var_raw = [&](const u32x4 (&w)[CPL], bool ok) -> float {
+  auto var_raw = [&](const u32x4 (&w)[CPL]) -> float {
     float s = 0.f, q = 0.f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c)
@@ -352,7 +352,7 @@ void k_score_lagkv(ScoreLagArgs a) {
         s = __builtin_amdgcn_fdot2_f32_bf16(x, one2, s, false);
         q = __builtin_amdgcn_fdot2_f32_bf16(x, x, q, false);
       }
-    return finish_var(s, q, ok);
+    return finish_var(s, q);
   };
 
   const bool track_range = LAG && !fresh;
@@ -414,12 +414,12 @@ void k_score_lagkv(ScoreLagArgs a) {
               sums(a1, b1, e + 1);
             }
         }
-        v[u] = finish_var(sa, qa, ok[u]);
-        v[u + 1] = finish_var(sb, qb, ok[u + 1]);
+        v[u] = finish_var(sa, qa);
+        v[u + 1] = finish_var(sb, qb);
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < AH; ++u) v[u] = var_raw(raw[u], ok[u]);
+      for (int u = 0; u < AH; ++u) v[u] = var_raw(raw[u]);
     }
 #pragma unroll
     for (int u = 0; u < AH; ++u) {
