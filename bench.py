@@ -608,11 +608,13 @@ def online_step_report(E, w, reps):
     rebuild only) against the step that scores the chunk itself."""
     S = setup_hs(w, E)
     ms_scoring = _time_calls(lambda: E.epikv_evict_step(S.cfg, S.io), reps)
+    import torch
     ws_n = E.workspace_bytes(S.cfg, 0)
+    ws0 = torch.zeros(ws_n, dtype=torch.uint8, device=S.scores.device)
     io0 = E.make_step_io(
         0, None, 0, 0, S.n_cached, S.n_prefix, S.src, S.src_pt,
         S.src_pt.shape[1], S.dst, S.dst_pt, S.dst_pt.shape[1], S.scores,
-        S.ld_s, None, None, S.keep_idx, S.n_keep, S.status, S.cws, ws_n,
+        S.ld_s, None, None, S.keep_idx, S.n_keep, S.status, ws0, ws_n,
         dst_scores=S.dst_scores, src_pos=S.src_pos, dst_pos=S.dst_pos)
     ms_online = _time_calls(lambda: E.epikv_evict_step(S.cfg, io0), reps)
     r = {"workload": f"{w.name}: B={w.B}, C={w.chunk}, K={w.budget}",

@@ -66,7 +66,13 @@ typedef enum epikv_status {
 typedef enum epikv_seq_status {
   EPIKV_SEQ_OK = 0,
   EPIKV_SEQ_BUDGET = 1,     /* N > K but P + R >= K: no room for scored tokens */
-  EPIKV_SEQ_RANGE = 2       /* N, P, a kept index or a page id out of range */
+  EPIKV_SEQ_RANGE = 2,      /* N, P, a kept index or a page id out of range */
+  EPIKV_SEQ_SYNC = 3        /* the eviction step's selection of this sequence
+                               runs on several workgroups that wait for each
+                               other; one gave up waiting (about a second:
+                               the device was so busy with other work that
+                               they could not all run at once).  keep_idx
+                               is not valid; n_keep = -1. */
 } epikv_seq_status;
 
 /* Which per-token signal is scored. */
@@ -183,8 +189,9 @@ int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]);
 
 /* Device scratch that epikv_evict_step (and epikv_score) needs for a chunk
  * of `chunk` new tokens per sequence; for chunk = 0 (a step that only
- * selects and compacts) the compaction's scratch.  0 for an invalid cfg or
- * chunk < 0. */
+ * selects and compacts) the selection's scratch and the compaction's
+ * (epikv_select_workspace_bytes(cfg) + epikv_compact_workspace_bytes(cfg)).
+ * 0 for an invalid cfg or chunk < 0. */
 size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk);
 
 /* Device scratch of epikv_compact, epikv_compact_inplace and
@@ -298,6 +305,46 @@ int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
                  const int32_t* n_cached, const int32_t* n_prefix,
                  int32_t* keep_idx, int32_t* n_keep, int32_t* seq_status,
                  hipStream_t stream);
+
+/* Device scratch of epikv_select_ws: for batches of up to 128 sequences,
+ * per sequence 256 bytes (a marker, a flag, a count) and three histograms
+ * of 2048 uint32 bins, B*24832 bytes, then 2048 bytes (two counts per
+ * workgroup, at most 256 workgroups), rounded up to 256; 0 for a larger
+ * batch (never split) or an invalid cfg. */
+size_t epikv_select_workspace_bytes(const epikv_cfg* cfg);
+
+/*
+ * epikv_select_ws -- epikv_select with device scratch, so that one
+ * sequence's selection can be split over several workgroups (Sec. 3.1,
+ * Sec. 3.3, App. D; the results are those of epikv_select, bit for bit).
+ *
+ * Worth it when the batch is too small to fill the device with one
+ * workgroup per sequence (a single long prefill, a small decode batch):
+ * each sequence's positions are cut into slices of 1024 to 16384, one per
+ * workgroup, as few per workgroup as keep the grid within one workgroup
+ * per compute unit; rows that one workgroup covers anyway, and batches
+ * where the grid would not fit, run epikv_select's kernel.  The workgroups of a
+ * sequence wait for each other between the radix passes; if they cannot all
+ * be resident at once because other work holds the device for about a
+ * second, the sequence is flagged EPIKV_SEQ_SYNC (n_keep = -1) instead of
+ * waiting longer.
+ *
+ * workspace: epikv_select_workspace_bytes(cfg) bytes of device memory,
+ * 16-byte aligned (EPIKV_EALIGN), overlapping none of the other arguments
+ * (EPIKV_EALIAS); EPIKV_EWORKSPACE if it is missing or too small (it may be
+ * NULL when that size is 0).  Between calls it carries the selection's
+ * cleared scratch, so that no clearing launch is needed: reuse it unchanged
+ * from one call to the next.  Any contents are accepted (a first use, or
+ * scratch changed in between, is recognised by a 64-bit marker; that call
+ * runs one workgroup per sequence and leaves the scratch cleared), and the
+ * call may be captured in a HIP graph.  Calls that share a workspace must
+ * not overlap in time.  Other arguments and errors as for epikv_select.
+ */
+int epikv_select_ws(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
+                    const int32_t* n_cached, const int32_t* n_prefix,
+                    int32_t* keep_idx, int32_t* n_keep, int32_t* seq_status,
+                    void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
 
 /*
  * epikv_compact -- order-preserving rebuild of the cache (App. H).
@@ -437,7 +484,11 @@ typedef struct epikv_step_io {
  * was scored as it was generated (epikv_score_tokens) and its score is
  * already frozen in `scores`: select and compact only.  hidden, state_in
  * and state_out are then not used (may be NULL), and the workspace needs
- * epikv_workspace_bytes(cfg, 0) = epikv_compact_workspace_bytes(cfg) bytes.
+ * epikv_workspace_bytes(cfg, 0) bytes.
+ * The selection runs epikv_select_ws's kernels with their scratch at the
+ * start of the workspace, where it is kept from one step to the next (when
+ * the chunk lies inside the recency window it runs epikv_select's instead,
+ * beside the scoring).
  */
 int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                      hipStream_t stream);
@@ -463,8 +514,8 @@ int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
  * capture.  `stream` must belong to the calling thread's current device
  * (else EPIKV_EINVAL_PARAM); the address lookup failing returns
  * EPIKV_ELAUNCH.  Every call on one GPU shares its array, which keeps the
- * last call's contents (the step writes what it reads, so nothing needs
- * clearing): calls that overlap in time on one GPU -- on two streams, or
+ * last call's contents (the step writes what it reads, apart from the
+ * selection's scratch, which each call leaves cleared for the next): calls that overlap in time on one GPU -- on two streams, or
  * from two threads -- race and must not be issued.
  */
 int epikv_evict_step_noalloc(const epikv_cfg* cfg, const epikv_step_io* io,

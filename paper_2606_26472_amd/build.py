@@ -32,7 +32,7 @@ PROBE_SOURCES = ["copy_probe.hip"]
 
 SOURCES = ["epikv_api.hip", "score_hs.hip", "score_lagkv.hip", "zscore.hip",
            "select.hip", "compact.hip", "compact_inplace.hip", "score_tokens.hip",
-           "score_select.hip", "noalloc.hip"]
+           "score_select.hip", "select_multi.hip", "noalloc.hip"]
 
 ARCH = "gfx950"
 CXXFLAGS = [

@@ -403,6 +403,22 @@ int check_select(const epikv_cfg* c, const float* scores, int64_t ld_s, const in
   return EPIKV_OK;
 }
 
+// The split selection's scratch must not overlap what the selection reads
+// or writes.
+int check_select_scratch(const epikv_cfg* c, const float* scores, int64_t ld_s,
+                         const int32_t* n_cached, const int32_t* n_prefix,
+                         const int32_t* keep_idx, const int32_t* n_keep,
+                         const int32_t* seq_status, const void* ws) {
+  const size_t n = select_scratch_bytes(c->batch);
+  if (n == 0) return EPIKV_OK;
+  const size_t B = (size_t)c->batch;
+  if (overlap(ws, n, scores, B * (size_t)ld_s * 4) || overlap(ws, n, n_cached, B * 4) ||
+      overlap(ws, n, n_prefix, B * 4) || overlap(ws, n, keep_idx, B * (size_t)c->budget * 4) ||
+      overlap(ws, n, n_keep, B * 4) || overlap(ws, n, seq_status, B * 4))
+    return EPIKV_EALIAS;
+  return EPIKV_OK;
+}
+
 SelectArgs select_args(const epikv_cfg* c, const float* scores, int64_t ld_s, const int32_t* n_cached,
                        const int32_t* n_prefix, int32_t* keep_idx, int32_t* n_keep,
                        int32_t* seq_status, int min_n) {
@@ -648,8 +664,9 @@ EPIKV_EXPORT int epikv_state_layout(const epikv_cfg* cfg, size_t offsets[5]) {
 
 EPIKV_EXPORT size_t epikv_workspace_bytes(const epikv_cfg* cfg, int32_t chunk) {
   if (check_cfg(cfg) || chunk < 0) return 0;
-  if (chunk == 0) return compact_ws_bytes(cfg);  // a step without scoring
-  return sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk) + compact_ws_bytes(cfg);
+  const size_t fixed = select_scratch_bytes(cfg->batch) + compact_ws_bytes(cfg);
+  if (chunk == 0) return fixed;  // a step without scoring
+  return fixed + sig_bytes(cfg, chunk) + partial_bytes(cfg, chunk);
 }
 
 EPIKV_EXPORT size_t epikv_compact_workspace_bytes(const epikv_cfg* cfg) {
@@ -712,6 +729,30 @@ EPIKV_EXPORT int epikv_select(const epikv_cfg* cfg, const float* scores, int64_t
       select_args(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status, 0), stream));
 }
 
+EPIKV_EXPORT size_t epikv_select_workspace_bytes(const epikv_cfg* cfg) {
+  if (check_cfg(cfg)) return 0;
+  return select_scratch_bytes(cfg->batch);
+}
+
+EPIKV_EXPORT int epikv_select_ws(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
+                                 const int32_t* n_cached, const int32_t* n_prefix,
+                                 int32_t* keep_idx, int32_t* n_keep, int32_t* seq_status,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = check_select(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status);
+  if (st) return st;
+  const size_t need = select_scratch_bytes(cfg->batch);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need) return EPIKV_EWORKSPACE;
+    if (!aligned16(workspace)) return EPIKV_EALIGN;
+    st = check_select_scratch(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status,
+                              workspace);
+    if (st) return st;
+  }
+  const SelectArgs a =
+      select_args(cfg, scores, ld_s, n_cached, n_prefix, keep_idx, n_keep, seq_status, 0);
+  return launched(need > 0 ? launch_select_groups(a, workspace, stream) : launch_select(a, stream));
+}
+
 EPIKV_EXPORT int epikv_compact(const epikv_cfg* cfg, const epikv_pool* src, const int32_t* src_pt,
                                int64_t ld_src_pt, const epikv_pool* dst, const int32_t* dst_pt,
                                int64_t ld_dst_pt, const int32_t* keep_idx, const int32_t* n_keep,
@@ -770,19 +811,25 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
   if (!io->workspace || io->workspace_bytes < epikv_workspace_bytes(cfg, io->chunk))
     return EPIKV_EWORKSPACE;
   if (!aligned16(io->workspace)) return EPIKV_EALIGN;
+  // Workspace: the selection's scratch first (at a place that does not
+  // depend on the chunk, since it is kept from one call to the next), then
+  // the signal, the Lag-KV partial sums and the compaction's scratch.
+  void* ws_select = io->workspace;
+  const size_t sel_bytes = select_scratch_bytes(cfg->batch);
+  char* ws = (char*)io->workspace + sel_bytes;
+  const size_t ws_rest = io->workspace_bytes - sel_bytes;
   if (scoring) {
     st = check_score(cfg, io->chunk, io->hidden, io->ld_tok, io->ld_seq, &io->src, io->src_pt,
-                     io->ld_src_pt, io->n_cached, io->state_in, io->state_out,
-                     (float*)io->workspace, io->workspace, io->workspace_bytes, false);
+                     io->ld_src_pt, io->n_cached, io->state_in, io->state_out, (float*)ws, ws,
+                     ws_rest, false);
     if (st) return st;
-    st = check_zscore(cfg, io->chunk, (const float*)io->workspace, io->n_cached, io->state_in,
+    st = check_zscore(cfg, io->chunk, (const float*)ws, io->n_cached, io->state_in,
                       io->state_out, io->scores, io->ld_s);
     if (st) return st;
   }
   st = check_select(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix, io->keep_idx, io->n_keep,
                     io->seq_status);
   if (st) return st;
-  char* ws = (char*)io->workspace;
   char* ws_offsets =
       scoring ? ws + sig_bytes(cfg, io->chunk) + partial_bytes(cfg, io->chunk) : ws;
   // The scores are compacted only when the caller asks for them (out of
@@ -804,6 +851,9 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                        io->src_pos, io->dst_pos, io->ld_s, ws_offsets, compact_ws_bytes(cfg));
   }
   if (st) return st;
+  st = check_select_scratch(cfg, io->scores, io->ld_s, io->n_cached, io->n_prefix, io->keep_idx,
+                            io->n_keep, io->seq_status, ws_select);
+  if (st) return st;
   const size_t ws_state = state_layout(cfg).total;
   if (scoring && (overlap(io->workspace, io->workspace_bytes, io->state_in, ws_state) ||
                   overlap(io->workspace, io->workspace_bytes, io->state_out, ws_state)))
@@ -817,7 +867,7 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
                                     io->scores, io->ld_s, nullptr);
   bool selected = false;  // the select stage is on the stream
   if (!scoring) {
-    st = launched(launch_select(sel, stream));
+    st = launched(launch_select_groups(sel, ws_select, stream));
     if (st) return st;
     selected = true;
   } else if (cfg->signal == EPIKV_SIGNAL_HS) {
@@ -840,7 +890,7 @@ EPIKV_EXPORT int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
     if (st) return st;
     st = launched(launch_zscore(zs, stream));
     if (st) return st;
-    st = launched(launch_select(sel, stream));
+    st = launched(launch_select_groups(sel, ws_select, stream));
     if (st) return st;
   }
   if (io->in_place) {

@@ -126,6 +126,17 @@ struct SelectArgs {
   int32_t* seq_status;
 };
 
+// One sequence's selection split over `groups` workgroups (select_multi.hip).
+// scratch: per sequence kSelSeqWords words -- a 256-byte head (the 64-bit
+// marker that the rest is clear, a give-up flag, a join count), then the
+// three radix passes' histograms of 2048 bins -- followed by two words per
+// workgroup of the grid (each zeroed by its workgroup first).
+struct SelectMultiArgs {
+  SelectArgs sel;
+  uint32_t* scratch;
+  int32_t groups;
+};
+
 struct CompactArgs {
   const char* src;
   int64_t s_layer, s_kv, s_page, s_npages;
@@ -264,6 +275,11 @@ hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r,
                               hipStream_t s);
 hipError_t launch_zscore(const ZscoreArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+// The eviction step's selection: several workgroups per sequence when the
+// batch is too small to fill the device with one each (scratch of
+// select_scratch_bytes(B), kept between calls), else launch_select.
+hipError_t launch_select_groups(const SelectArgs& a, void* scratch, hipStream_t s);
+size_t select_scratch_bytes(int B);
 // Selection and hidden-state scoring in one launch; valid only when
 // select_score_fusable (the chunk lies inside the recency window).
 bool select_score_fusable(const SelectArgs& sel, const ScoreHsArgs& sc);
@@ -281,6 +297,11 @@ constexpr int kZscoreTile = 64;          // tokens per zscore workgroup (one per
 constexpr int kZscoreThreads = 1024;     // 16 wavefronts: one signal row each
 constexpr int kTokMaxRow = 4096;         // fused per-token scorer: widest hidden row
 constexpr int kSelectThreads = 1024;
+constexpr int kSelHeadWords = 64;                         // marker, flag, join count
+constexpr uint32_t kSelMarkLo = 0x9E3779B9u;              // "this scratch is clear"
+constexpr uint32_t kSelMarkHi = 0x7F4A7C15u;
+constexpr int kSelSeqWords = kSelHeadWords + 3 * 2048;    // per-sequence scratch words
+constexpr int kSelMaxGrid = 256;  // workgroups of a multi-workgroup selection, at most
 constexpr int kCompactThreads = 256;      // resolve kernel; in-place move workgroups
 constexpr int64_t kCompactGridX = 1 << 24;  // gather workgroups per grid row
 constexpr int kCompactWaves = kCompactThreads / 64;  // walks per in-place move workgroup

@@ -11,7 +11,9 @@
 // current, and kept in `g_scratch`.  Only that address is ever handed to a
 // kernel.  Every call on one GPU shares the array and it keeps the last
 // call's contents; the step's kernels write every scratch word before they
-// read it, so nothing needs clearing.  Calls that overlap in time on one GPU
+// read it, except the selection's histograms, which each call leaves
+// cleared for the next (recognised by a marker; the array starts zeroed,
+// without the marker, so the first call on a device clears them itself).  Calls that overlap in time on one GPU
 // (two streams, two threads) race on it.
 #include <mutex>
 

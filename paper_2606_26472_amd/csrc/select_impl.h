@@ -106,6 +106,35 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return pre + x - v;
 }
 
+// The digit holding the need-th largest key of a histogram of nb bins in
+// LDS (nb a multiple of the workgroup size), and how many keys lie in
+// higher digits; both land in *digit / *above.  Thread t owns the bpt bins
+// just below nb - t*bpt (descending order), so the inclusive scan counts
+// keys whose digit is >= its lowest bin.
+__device__ __forceinline__ void find_digit(const uint32_t* hist, int nb, uint32_t need,
+                                           uint32_t* wsum, uint32_t* digit, uint32_t* above_out) {
+  const int bpt = nb / kSelectThreads;
+  const int top = nb - 1 - (int)threadIdx.x * bpt;
+  uint32_t local = 0u;
+  for (int q = 0; q < bpt; ++q) local += hist[top - q];
+  const uint32_t incl = block_inclusive_scan(local, wsum);
+  const uint32_t excl = incl - local;
+  if (excl < need && need <= incl) {
+    uint32_t above = excl;
+    int d = top - bpt + 1;
+    for (int q = 0; q < bpt; ++q) {
+      const uint32_t h = hist[top - q];
+      if (above + h >= need) {
+        d = top - q;
+        break;
+      }
+      above += h;
+    }
+    *digit = (uint32_t)d;
+    *above_out = above;
+  }
+}
+
 // KPT > 0: positions [tid*KPT, (tid+1)*KPT) have their keys in registers.
 // KPT == 0: keys are recomputed from global memory in every sweep.
 template <int KPT>
@@ -194,28 +223,7 @@ __device__ __forceinline__ void select_seq(const SelectArgs& a, int b) {
       }
     }
     __syncthreads();
-    // Thread t owns the bpt bins just below nb - t*bpt (descending order),
-    // so the inclusive scan counts keys whose digit is >= its lowest bin.
-    const int bpt = nb / kSelectThreads;
-    const int top = nb - 1 - tid * bpt;
-    uint32_t local = 0u;
-    for (int q = 0; q < bpt; ++q) local += hist[top - q];
-    const uint32_t incl = block_inclusive_scan(local, wsum);
-    const uint32_t excl = incl - local;
-    if (excl < need && need <= incl) {
-      uint32_t above = excl;
-      int d = top - bpt + 1;
-      for (int q = 0; q < bpt; ++q) {
-        const uint32_t h = hist[top - q];
-        if (above + h >= need) {
-          d = top - q;
-          break;
-        }
-        above += h;
-      }
-      sel_digit = (uint32_t)d;
-      sel_above = above;
-    }
+    find_digit(hist, nb, need, wsum, &sel_digit, &sel_above);
     __syncthreads();
     prefix |= sel_digit << shift;
     mask |= dmask << shift;

@@ -28,6 +28,7 @@ EPIKV_ELAUNCH = -7
 SEQ_OK = 0
 SEQ_BUDGET = 1
 SEQ_RANGE = 2
+SEQ_SYNC = 3
 COMPACT_OUT_OF_PLACE, COMPACT_IN_PLACE, COMPACT_REMAP = 0, 1, 2
 
 SIGNAL_HS = 0
@@ -45,7 +46,8 @@ EXPORTED = ("epikv_default_cfg", "epikv_strerror", "epikv_check_cfg",
             "epikv_state_bytes", "epikv_state_layout",
             "epikv_workspace_bytes", "epikv_compact_workspace_bytes",
             "epikv_state_init", "epikv_score", "epikv_score_tokens",
-            "epikv_zscore", "epikv_select", "epikv_compact",
+            "epikv_zscore", "epikv_select", "epikv_select_workspace_bytes",
+            "epikv_select_ws", "epikv_compact",
             "epikv_compact_inplace", "epikv_compact_remap",
             "epikv_evict_step", "epikv_evict_step_noalloc")
 
@@ -125,6 +127,9 @@ def lib() -> ctypes.CDLL:
         "epikv_score_tokens": (ctypes.c_int, [cfgp, i32, ctypes.POINTER(P), i64,
                                               i64, P, P, P, P, i64, P]),
         "epikv_select": (ctypes.c_int, [cfgp, P, i64, P, P, P, P, P, P]),
+        "epikv_select_workspace_bytes": (sz, [cfgp]),
+        "epikv_select_ws": (ctypes.c_int, [cfgp, P, i64, P, P, P, P, P, P,
+                                           sz, P]),
         "epikv_compact": (ctypes.c_int, [cfgp, poolp, P, i64, poolp, P, i64,
                                          P, P, P, P, P, P, i64, P, P, sz, P]),
         "epikv_compact_inplace": (ctypes.c_int, [cfgp, poolp, P, i64, P, P,
@@ -159,6 +164,17 @@ def _ptr(t):
     if isinstance(t, int):
         return t
     return t.data_ptr()
+
+
+def _ws(t, nbytes):
+    """Address of a workspace tensor, refusing one smaller than the size
+    that will be declared to the library (it would write past its end)."""
+    if t is not None and not isinstance(t, int):
+        have = t.numel() * t.element_size()
+        if have < int(nbytes):
+            raise ValueError(f"workspace tensor holds {have} bytes, "
+                             f"{int(nbytes)} declared")
+    return _ptr(t)
 
 
 def _stream(stream):
@@ -204,6 +220,10 @@ def compact_workspace_bytes(cfg: Cfg) -> int:
     return int(lib().epikv_compact_workspace_bytes(ctypes.byref(cfg)))
 
 
+def select_workspace_bytes(cfg: Cfg) -> int:
+    return int(lib().epikv_select_workspace_bytes(ctypes.byref(cfg)))
+
+
 def pool_of(t) -> Pool:
     """epikv_pool describing a tensor laid out [L][2][n_pages][page][H][d]."""
     es = t.element_size()
@@ -237,7 +257,8 @@ def epikv_score(cfg: Cfg, chunk: int, hidden=None, ld_tok=0, ld_seq=0,
         ctypes.byref(cfg), int(chunk), arr, int(ld_tok), int(ld_seq),
         ctypes.byref(pool) if pool is not None else None, _ptr(page_table),
         int(ld_pt), _ptr(n_cached), _ptr(state_in), _ptr(state_out),
-        _ptr(sig), _ptr(workspace), int(workspace_bytes_), _stream(stream)),
+        _ptr(sig), _ws(workspace, workspace_bytes_), int(workspace_bytes_),
+        _stream(stream)),
         "epikv_score")
 
 
@@ -266,6 +287,17 @@ def epikv_select(cfg: Cfg, scores, ld_s, n_cached, n_prefix, keep_idx,
         _stream(stream)), "epikv_select")
 
 
+def epikv_select_ws(cfg: Cfg, scores, ld_s, n_cached, n_prefix, keep_idx,
+                    n_keep, seq_status, workspace=None, workspace_bytes_=0,
+                    stream=None):
+    _check(lib().epikv_select_ws(
+        ctypes.byref(cfg), _ptr(scores), int(ld_s), _ptr(n_cached),
+        _ptr(n_prefix), _ptr(keep_idx), _ptr(n_keep), _ptr(seq_status),
+        _ws(workspace, workspace_bytes_), int(workspace_bytes_),
+        _stream(stream)),
+        "epikv_select_ws")
+
+
 def epikv_compact(cfg: Cfg, src: Pool, src_pt, ld_src_pt, dst: Pool, dst_pt,
                   ld_dst_pt, keep_idx, n_keep, src_scores=None,
                   dst_scores=None, src_pos=None, dst_pos=None, ld_s=0,
@@ -275,8 +307,9 @@ def epikv_compact(cfg: Cfg, src: Pool, src_pt, ld_src_pt, dst: Pool, dst_pt,
         ctypes.byref(cfg), ctypes.byref(src), _ptr(src_pt), int(ld_src_pt),
         ctypes.byref(dst), _ptr(dst_pt), int(ld_dst_pt), _ptr(keep_idx),
         _ptr(n_keep), _ptr(src_scores), _ptr(dst_scores), _ptr(src_pos),
-        _ptr(dst_pos), int(ld_s), _ptr(seq_status), _ptr(workspace),
-        int(workspace_bytes_), _stream(stream)),
+        _ptr(dst_pos), int(ld_s), _ptr(seq_status),
+        _ws(workspace, workspace_bytes_), int(workspace_bytes_),
+        _stream(stream)),
         "epikv_compact")
 
 
@@ -287,7 +320,7 @@ def epikv_compact_inplace(cfg: Cfg, pool: Pool, page_table, ld_pt, keep_idx,
     _check(lib().epikv_compact_inplace(
         ctypes.byref(cfg), ctypes.byref(pool), _ptr(page_table), int(ld_pt),
         _ptr(keep_idx), _ptr(n_keep), _ptr(scores), _ptr(pos), int(ld_s),
-        _ptr(seq_status), _ptr(workspace), int(workspace_bytes_),
+        _ptr(seq_status), _ws(workspace, workspace_bytes_), int(workspace_bytes_),
         _stream(stream)), "epikv_compact_inplace")
 
 
@@ -298,7 +331,7 @@ def epikv_compact_remap(cfg: Cfg, pool: Pool, page_table, ld_pt, keep_idx,
     _check(lib().epikv_compact_remap(
         ctypes.byref(cfg), ctypes.byref(pool), _ptr(page_table), int(ld_pt),
         _ptr(keep_idx), _ptr(n_keep), _ptr(scores), _ptr(pos), int(ld_s),
-        _ptr(seq_status), _ptr(workspace), int(workspace_bytes_),
+        _ptr(seq_status), _ws(workspace, workspace_bytes_), int(workspace_bytes_),
         _stream(stream)), "epikv_compact_remap")
 
 
@@ -330,7 +363,8 @@ def make_step_io(chunk, hidden, ld_tok, ld_seq, n_cached, n_prefix,
     io.state_in, io.state_out = _ptr(state_in), _ptr(state_out)
     io.keep_idx, io.n_keep = _ptr(keep_idx), _ptr(n_keep)
     io.seq_status = _ptr(seq_status)
-    io.workspace, io.workspace_bytes = _ptr(workspace), int(workspace_bytes_)
+    io.workspace = _ws(workspace, workspace_bytes_)
+    io.workspace_bytes = int(workspace_bytes_)
     io.in_place = int(in_place)   # False/True, or a COMPACT_* mode
     return io
 

@@ -97,7 +97,15 @@ def test_state_layout_sizes(E):
     assert E.workspace_bytes(lag, 256) >= 4 * 8 * 256 + 4 * 8 * 64 * 256
     assert E.workspace_bytes(c, -1) == 0
     # a step that only selects and compacts needs the compaction's scratch
-    assert E.workspace_bytes(c, 0) == E.compact_workspace_bytes(c)
+    # and, for batches of up to 128 sequences (the selection may then split
+    # a sequence over several workgroups), per sequence a 256-byte head and
+    # three 2048-bin histograms plus two words for each of up to 256
+    # workgroups
+    sel = 32 * (256 + 3 * 2048 * 4) + 256 * 8
+    assert E.select_workspace_bytes(c) == sel
+    assert E.workspace_bytes(c, 0) == E.compact_workspace_bytes(c) + sel
+    big = E.default_cfg(batch=129)
+    assert E.workspace_bytes(big, 0) == E.compact_workspace_bytes(big)
     # records, per-sequence info, four page arrays per sequence
     assert E.compact_workspace_bytes(c) == 16 * 32 * 4096 + 256 + 16 * 32 * 256
     assert E.workspace_bytes(c, 128) >= E.compact_workspace_bytes(c) \
@@ -190,6 +198,23 @@ def test_zscore_select_compact_validation(E):
              None) == E.EPIKV_EINVAL_NULL
     assert s(ctypes.byref(c), A, 0, A, A, A, A, A,
              None) == E.EPIKV_EINVAL_SHAPE
+    # the split selection: workspace missing, too small, misaligned, or
+    # overlapping an output (scores at A, the outputs at 2A..)
+    sw = L.epikv_select_ws
+    nws = E.select_workspace_bytes(c)
+    assert nws == 2 * (256 + 3 * 2048 * 4) + 256 * 8
+    W = 8 * A
+    assert sw(ctypes.byref(c), A, 100, A, A, 2 * A, 3 * A, 4 * A, None, 0,
+              None) == E.EPIKV_EWORKSPACE
+    assert sw(ctypes.byref(c), A, 100, A, A, 2 * A, 3 * A, 4 * A, W,
+              nws - 1, None) == E.EPIKV_EWORKSPACE
+    assert sw(ctypes.byref(c), A, 100, A, A, 2 * A, 3 * A, 4 * A, W + 4,
+              nws, None) == E.EPIKV_EALIGN
+    assert sw(ctypes.byref(c), A, 100, 5 * A, 6 * A, 2 * A, 3 * A, 4 * A,
+              2 * A + 256, nws, None) == E.EPIKV_EALIAS
+    assert sw(ctypes.byref(c), A, 0, A, A, A, A, A, W, nws,
+              None) == E.EPIKV_EINVAL_SHAPE
+    assert E.select_workspace_bytes(E.default_cfg(batch=129)) == 0
     cp = L.epikv_compact
     src = E.Pool(A, 1 << 30, 1 << 29, 32768, 100)
     dst = E.Pool(2 * A, 1 << 30, 1 << 29, 32768, 100)

@@ -175,10 +175,27 @@ def test_zscore_matches_oracle(E, mode, C):
 # ---------------------------------------------------------------------------
 # select: Sec. 3.1, Sec. 3.3, App. D
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("ld_s", [65536, 80000, 3000])
-def test_select_matches_oracle_bit_exact(E, ld_s):
+def _select(E, entry, cfg, scores, ld_s, n_cached, n_prefix, keep, n_keep,
+            status):
+    """epikv_select, or epikv_select_ws (one sequence split over several
+    workgroups when the batch is small) with a workspace of garbage."""
     import torch
-    print(f"select ld_s={ld_s}", flush=True)
+    if entry == "select":
+        E.epikv_select(cfg, scores, ld_s, n_cached, n_prefix, keep, n_keep,
+                       status)
+        return
+    n = E.select_workspace_bytes(cfg)
+    ws = torch.randint(-2**31, 2**31 - 1, (max(n, 16) // 4,),
+                       dtype=torch.int32, device="cuda")
+    E.epikv_select_ws(cfg, scores, ld_s, n_cached, n_prefix, keep, n_keep,
+                      status, ws, n)
+
+
+@pytest.mark.parametrize("entry", ["select", "select_ws"])
+@pytest.mark.parametrize("ld_s", [65536, 80000, 3000])
+def test_select_matches_oracle_bit_exact(E, ld_s, entry):
+    import torch
+    print(f"{entry} ld_s={ld_s}", flush=True)
     g = synth.rng(300 + ld_s)
     K = 1024
     # ld_s picks the kernel variant: keys in registers (<= 64 Ki positions)
@@ -199,8 +216,8 @@ def test_select_matches_oracle_bit_exact(E, ld_s):
     keep = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
     n_keep = torch.zeros(B, dtype=torch.int32, device="cuda")
     status = torch.full((B,), 9, dtype=torch.int32, device="cuda")
-    E.epikv_select(cfg, dev(sc), ld_s, dev(np.array(Ns, np.int32)),
-                   dev(np.array(Ps, np.int32)), keep, n_keep, status)
+    _select(E, entry, cfg, dev(sc), ld_s, dev(np.array(Ns, np.int32)),
+            dev(np.array(Ps, np.int32)), keep, n_keep, status)
     _sync()
     keep, n_keep, status = host(keep), host(n_keep), host(status)
     R = O.default_recent(K)
@@ -219,22 +236,100 @@ def test_select_matches_oracle_bit_exact(E, ld_s):
         assert np.all(keep[b, ref.size:] == -5)
 
 
-def test_select_all_equal_scores_keeps_lowest_positions(E):
+@pytest.mark.parametrize("entry", ["select", "select_ws"])
+@pytest.mark.parametrize("N", [3000, 65536])
+def test_select_all_equal_scores_keeps_lowest_positions(E, N, entry):
+    # every eligible key ties: the kept ones are the lowest positions, also
+    # when the positions are split over several workgroups
     import torch
-    B, K, N = 2, 256, 3000
+    B, K = 2, 256
     sc = np.zeros((B, N), dtype=np.float32)
     sc[1] = np.nan
     cfg = E.default_cfg(batch=B, budget=K)
     keep = torch.zeros((B, K), dtype=torch.int32, device="cuda")
     n_keep = torch.zeros(B, dtype=torch.int32, device="cuda")
-    st = torch.zeros(B, dtype=torch.int32, device="cuda")
-    E.epikv_select(cfg, dev(sc), N, dev(np.full(B, N, np.int32)),
-                   dev(np.zeros(B, np.int32)), keep, n_keep, st)
+    st = torch.full((B,), 9, dtype=torch.int32, device="cuda")
+    _select(E, entry, cfg, dev(sc), N, dev(np.full(B, N, np.int32)),
+            dev(np.zeros(B, np.int32)), keep, n_keep, st)
     _sync()
     R = 64
     exp = np.concatenate([np.arange(K - R), np.arange(N - R, N)])
+    assert np.array_equal(host(st), [E.SEQ_OK] * B)
+    assert np.array_equal(host(n_keep), [K] * B)
     for b in range(B):
         assert np.array_equal(host(keep)[b], exp)
+
+
+@pytest.mark.parametrize("B,ld_s,K", [(1, 65536, 8192), (1, 3000, 1024),
+                                      (32, 32896, 4096), (4, 80000, 8192),
+                                      (1, 70000, 300), (128, 2048, 256)])
+def test_select_split_matches_oracle_bit_exact(E, B, ld_s, K):
+    """epikv_select_ws at the batch shapes that split a sequence: a single
+    long prefill (64 workgroups of one key per thread), the decode batch of
+    32 ragged sequences (5 workgroups of 8), a ragged tail, slices past N,
+    and the biggest batch that still splits."""
+    import torch
+    print(f"select_ws B={B} ld_s={ld_s} K={K}", flush=True)
+    g = synth.rng(900 + B + ld_s + K)
+    Ns = g.integers(max(K + 1, ld_s // 4), ld_s + 1, B)
+    Ns[0] = ld_s
+    if B > 2:
+        Ns[1] = K          # keep all
+        Ns[2] = ld_s // 3  # short row: trailing workgroups see no position
+    Ps = g.integers(0, max(1, K // 8), B)
+    sc = np.zeros((B, ld_s), dtype=np.float32)
+    for b in range(B):
+        s = synth.old_scores(g, ld_s, ties=(b % 2 == 0))
+        s[g.integers(0, ld_s, 20)] = np.nan
+        s[g.integers(0, ld_s, 20)] = -0.0
+        s[g.integers(0, ld_s, 5)] = -np.inf
+        sc[b] = s
+    cfg = E.default_cfg(batch=B, budget=K)
+    keep = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
+    n_keep = torch.zeros(B, dtype=torch.int32, device="cuda")
+    status = torch.full((B,), 9, dtype=torch.int32, device="cuda")
+    d_sc, d_n, d_p = (dev(sc), dev(Ns.astype(np.int32)),
+                      dev(Ps.astype(np.int32)))
+    _select(E, "select_ws", cfg, d_sc, ld_s, d_n, d_p, keep, n_keep, status)
+    _sync()
+    # a second call on the same (now dirty) workspace gives the same result
+    keep2 = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
+    n2 = torch.zeros(B, dtype=torch.int32, device="cuda")
+    st2 = torch.full((B,), 9, dtype=torch.int32, device="cuda")
+    n = E.select_workspace_bytes(cfg)
+    ws = torch.empty(n // 4, dtype=torch.int32, device="cuda")
+    for kk, nn, ss in ((keep, n_keep, status), (keep2, n2, st2)):
+        kk.fill_(-5)
+        E.epikv_select_ws(cfg, d_sc, ld_s, d_n, d_p, kk, nn, ss, ws, n)
+    _sync()
+    assert torch.equal(keep, keep2) and torch.equal(n_keep, n2) \
+        and torch.equal(status, st2)
+    R = O.default_recent(K)
+
+    def check(keep, n_keep, status, sc, Ns, Ps):
+        keep, n_keep, status = host(keep), host(n_keep), host(status)
+        for b in range(B):
+            ref = O.select_keep(sc[b, :Ns[b]], int(Ps[b]), K, R)
+            assert status[b] == E.SEQ_OK, b
+            assert n_keep[b] == ref.size, b
+            assert np.array_equal(keep[b, :ref.size], ref), b
+            assert np.all(keep[b, ref.size:] == -5)
+
+    check(keep, n_keep, status, sc, Ns, Ps)
+    # The workspace carries the cleared scratch from call to call: further
+    # calls on it with other scores, lengths and prefixes, and with a
+    # shorter row (a different split), are exact too.
+    for rep in range(3):
+        ld2 = ld_s if rep < 2 else max(K + 1, ld_s // 2)
+        sc2 = np.stack([synth.old_scores(g, ld2, ties=(rep == 1))
+                        for _ in range(B)])
+        Ns2 = g.integers(min(ld2, K + 1), ld2 + 1, B)
+        Ps2 = g.integers(0, max(1, K // 8), B)
+        kk = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
+        E.epikv_select_ws(cfg, dev(sc2), ld2, dev(Ns2.astype(np.int32)),
+                          dev(Ps2.astype(np.int32)), kk, n2, st2, ws, n)
+        _sync()
+        check(kk, n2, st2, sc2, Ns2, Ps2)
 
 
 # ---------------------------------------------------------------------------
