@@ -159,6 +159,9 @@ def setup_hs(w: synth.Workload, E, log_every=True):
     S.ws = torch.zeros(S.ws_bytes, dtype=torch.uint8, device=dev)
     S.cws_bytes = E.compact_workspace_bytes(cfg)
     S.cws = torch.zeros(S.cws_bytes, dtype=torch.uint8, device=dev)
+    S.sel_ws_bytes = E.select_workspace_bytes(cfg)
+    S.sel_ws = torch.zeros(max(S.sel_ws_bytes, 16), dtype=torch.uint8,
+                           device=dev)
 
     t0 = time.time()
     row = H * d
@@ -185,8 +188,9 @@ def setup_hs(w: synth.Workload, E, log_every=True):
         S.state_in, S.state_out, S.keep_idx, S.n_keep, S.status, S.ws,
         S.ws_bytes, dst_scores=S.dst_scores, src_pos=S.src_pos,
         dst_pos=S.dst_pos)
-    S.sig = S.ws[:E.n_sig(cfg) * B * C * 4].view(torch.float32).view(
-        E.n_sig(cfg), B, C)
+    # (a buffer of its own: the step keeps the selection's scratch at the
+    # start of its workspace from one call to the next)
+    S.sig = torch.zeros((E.n_sig(cfg), B, C), device=dev)
     S.score_call = lambda: E.epikv_score(
         cfg, C, S.hidden_ptrs, D, C * D, state_in=S.state_in,
         state_out=S.state_out, sig=S.sig)
@@ -213,6 +217,9 @@ def _step_buffers(S, E, cfg, w, lengths, src_pt, dst_pt, n_src, n_dst, dev):
     S.ws = torch.zeros(S.ws_bytes, dtype=torch.uint8, device=dev)
     S.cws_bytes = E.compact_workspace_bytes(cfg)
     S.cws = torch.zeros(S.cws_bytes, dtype=torch.uint8, device=dev)
+    S.sel_ws_bytes = E.select_workspace_bytes(cfg)
+    S.sel_ws = torch.zeros(max(S.sel_ws_bytes, 16), dtype=torch.uint8,
+                           device=dev)
     L, H, d, page = w.n_layers, w.n_kv_heads, w.head_dim, w.page_size
     S.src = E.pool_of(S.src_pool.view(L, 2, n_src, page, H, d))
     S.dst = E.pool_of(S.dst_pool.view(L, 2, n_dst, page, H, d))
@@ -330,7 +337,9 @@ def setup_prefill(w: synth.Workload, E):
                              device=dev)
     E.epikv_state_init(cfg, S.state_in)
     S.state_out = torch.zeros_like(S.state_in)
-    S.sig = S.ws[:nb * T * 4].view(torch.float32).view(nb, 1, T)
+    # (a buffer of its own: the step keeps the selection's scratch at the
+    # start of its workspace from one call to the next)
+    S.sig = torch.zeros((nb, 1, T), device=dev)
     S.score_call = lambda: E.epikv_score(
         cfg, T, S.hidden_ptrs, D, T * D, state_in=S.state_in,
         state_out=S.state_out, sig=S.sig)
@@ -355,8 +364,9 @@ def run_stages(E, S, w, events=None):
                    S.scores, S.ld_s)
     if events:
         events[2].record()
-    E.epikv_select(S.cfg, S.scores, S.ld_s, S.n_cached, S.n_prefix,
-                   S.keep_idx, S.n_keep, S.status)
+    E.epikv_select_ws(S.cfg, S.scores, S.ld_s, S.n_cached, S.n_prefix,
+                      S.keep_idx, S.n_keep, S.status, S.sel_ws,
+                      S.sel_ws_bytes)
     if events:
         events[3].record()
     E.epikv_compact(S.cfg, S.src, S.src_pt, S.src_pt.shape[1], S.dst,

@@ -97,7 +97,8 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
 }
 
 // Sum of v over the workgroup, the same in every thread (wtot: kWaves words
-// of LDS).
+// of LDS).  One barrier: callers alternate between two wtot buffers, so a
+// buffer is rewritten only after the barrier of the call in between.
 __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* wtot) {
   const int wave = threadIdx.x >> 6;
   v = wave_scan(v);
@@ -106,7 +107,6 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* wtot) {
   uint32_t t = 0u;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) t += wtot[w];
-  __syncthreads();  // wtot is reused
   return t;
 }
 
@@ -194,7 +194,7 @@ template <int KPT>
 __global__ __launch_bounds__(kSelectThreads) void k_select_multi(SelectMultiArgs m) {
   __shared__ __align__(16) uint32_t hist[2048];
   __shared__ uint32_t tab[2][KPT * kWaves];  // per (row of 1024, wavefront) counts
-  __shared__ uint32_t wtot[kWaves];
+  __shared__ uint32_t wtot[2][kWaves];
   __shared__ uint32_t bcast[8];
   const SelectArgs& a = m.sel;
   const int G = m.groups;
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_multi(SelectMultiArgs
         hist[i] = h;
         part += h;
       }
-      if (block_sum(part, wtot) == expect) break;
+      if (block_sum(part, wtot[spins & 1]) == expect) break;
       if (spins == kSpinLimit) {
         give_up(a, b, seq);
         return;
@@ -349,7 +349,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_multi(SelectMultiArgs
     mask |= dmask << shift;
     need -= bcast[1];
     expect = bcast[2];
-    __syncthreads();  // bcast is rewritten
+    // (bcast is next written by the next pass's search, barriers later)
   }
 
   // need = keys equal to T that are kept, lowest positions first; expect =
