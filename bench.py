@@ -999,7 +999,8 @@ def main():
     # a one-shot prefill
     dom = "compact" if stage_ms["compact"] >= stage_ms["score"] else "score"
     dom_gbps = ab[dom] / (stage_ms[dom] * 1e-3) / 1e9
-    dom_name = {"compact": "epikv_compact (k_compact_resolve + k_compact)",
+    dom_name = {"compact": "epikv_compact (k_compact_order + "
+                           "k_compact_resolve + k_compact)",
                 "score": ("epikv_score (k_score_lagkv + k_lag_reduce)"
                           if kind == "lagkv" else
                           "epikv_score (k_score_hs_wave)")}[dom]
