@@ -95,12 +95,13 @@ int lag_planes(const epikv_cfg* c) {
 }
 
 // Workgroups sharing the rows of one (sequence, plane) in the KV-vector
-// scorer: enough for about kLagWgWanted workgroups, each keeping at least
-// kLagAhead rows per wavefront.
+// scorer: enough for about kLagWgWanted workgroups, each wavefront keeping
+// at least its rows in flight busy.
 int lag_splits(const epikv_cfg* c, int chunk) {
+  const bool lag = uses_range(c->signal);
   const int64_t base = (int64_t)lag_planes(c) * c->batch;
   const int64_t s = (kLagWgWanted + base - 1) / base;
-  const int64_t cap = std::max<int64_t>(1, chunk / (kLagWaves * kLagAhead));
+  const int64_t cap = std::max<int64_t>(1, chunk / (lagkv_waves(lag) * lagkv_ahead(lag)));
   return (int)std::max<int64_t>(1, std::min(s, cap));
 }
 

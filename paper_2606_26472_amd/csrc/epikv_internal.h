@@ -305,34 +305,40 @@ constexpr int kSelMaxGrid = 256;  // workgroups of a multi-workgroup selection, 
 constexpr int kCompactThreads = 256;      // resolve kernel; in-place move workgroups
 constexpr int64_t kCompactGridX = 1 << 24;  // gather workgroups per grid row
 constexpr int kCompactWaves = kCompactThreads / 64;  // walks per in-place move workgroup
-constexpr int kLagWaves = 8;             // wavefronts per KV-vector scorer workgroup
-constexpr int kLagThreads = kLagWaves * 64;
-constexpr int kLagAhead = 4;             // rows a KV-scorer wavefront loads before using them (even)
 constexpr int kLagWgWanted = 512;        // split a plane's rows until this many workgroups
 constexpr int kLagPtCache = 1024;        // page-table entries a KV-scorer workgroup keeps in LDS
 
-// KV-vector scorer: wavefronts per row (segments of 64 lanes x 8 or 16
-// channels), and LDS: the range combine's tree -- half as many slots of
-// [2][H*d] floats as partial ranges (row slots x rows per wavefront; the
-// broadcast reuses slot 0) -- then kLagPtCache page-table entries.
-// 16-byte columns per lane: 2 for the raw signals' rows of 1024 channels
-// or more, else 1.
-__host__ __device__ inline int lagkv_cpl(int H, int d, bool lag) {
-  return (!lag && H * d / 8 >= 128) ? 2 : 1;
+// KV-vector scorer shapes (lag: a lag-normalised signal).  Wavefronts per
+// workgroup and rows each keeps in flight: 8 and 8 for the lag-normalised
+// signals, whose four registers of per-channel state allow four
+// wavefronts per SIMD; 16 and 4 for the raw signals, which fit eight.
+// A lane takes 4 words (8 channels, 16 bytes) of a row, so a row spans
+// H*d / 8 lanes; from 64 lanes on it is split into segments of 64 lanes,
+// one wavefront each.
+// LDS: the range slots (lag-normalised only; one [2][H*d] slot per row
+// slot, or per row of a wavefront for narrow rows), then the transposed
+// reduction's rows (row segments), then kLagPtCache page-table entries.
+__host__ __device__ constexpr int lagkv_waves(bool lag) { return lag ? 8 : 16; }
+__host__ __device__ constexpr int lagkv_threads(bool lag) { return 64 * lagkv_waves(lag); }
+__host__ __device__ constexpr int lagkv_ahead(bool lag) { return lag ? 8 : 4; }
+constexpr int kLagWords = 4;
+__host__ __device__ inline int lagkv_row_lanes(int H, int d, bool) { return H * d / (2 * kLagWords); }
+__host__ __device__ inline bool lagkv_wide(int H, int d, bool lag) {
+  return lagkv_row_lanes(H, d, lag) >= 64;
 }
 __host__ __device__ inline int lagkv_segments(int H, int d, bool lag) {
-  const int row_vec = H * d / 8;
-  const int per = 64 * lagkv_cpl(H, d, lag);
-  return row_vec >= per ? row_vec / per : 1;
+  const int lanes = lagkv_row_lanes(H, d, lag);
+  return lanes >= 64 ? lanes / 64 : 1;
 }
-// (the tree exists for the lag-normalised signals only: one column per lane)
-__host__ __device__ inline int lagkv_tree_floats(int H, int d) {
-  const int HD = H * d;
-  const int row_vec = HD / 8;
-  const int n_part = row_vec >= 64 ? kLagWaves / lagkv_segments(H, d, true)
-                                   : kLagWaves * (64 / row_vec);
-  return (n_part > 1 ? n_part / 2 : 1) * 2 * HD;
+__host__ __device__ inline int lagkv_range_floats(int H, int d) {
+  const int lanes = lagkv_row_lanes(H, d, true);
+  const int n_part = lanes >= 64 ? lagkv_waves(true) / lagkv_segments(H, d, true)
+                                 : lagkv_waves(true) * (64 / lanes);
+  return n_part * 2 * H * d;
 }
+// The transposed reduction's row of 64 (sum, sum of squares) pairs, with
+// 4 words of padding after every 8 lanes.
+constexpr int kRedRowWords = 64 * 2 + 8 * 4;
 size_t lagkv_lds_bytes(int H, int d, bool lag);
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this

@@ -10,30 +10,38 @@
 // out as the next chunk's reference; the first chunk of a stream, with no
 // previous chunk, is normalised by its own range.
 //
-// Kernel 1: one 512-thread workgroup per (sequence, used plane) -- a plane is
-// one (layer, K|V) of a used tensor, so signals of one tensor launch half as
-// many -- streaming the chunk's rows of that plane from the paged pool.  When
-// that gives too few workgroups to fill the GPU the rows are split between
-// `splits` workgroups, whose partial channel ranges the second kernel
-// combines; otherwise the workgroup writes the chunk's range itself.
-// A lane owns one 16-byte column = 8 channels of one head, so a head's
-// statistics reduce over d/8 lanes with DPP row operations.  A wavefront
+// Kernel 1: one workgroup per (sequence, used plane) -- a plane is one
+// (layer, K|V) of a used tensor, so signals of one tensor launch half as
+// many -- streaming the chunk's rows of that plane from the paged pool:
+// 512 threads for the lag-normalised signals (four registers of state per
+// channel), 1024 for the raw ones.  When that gives too few workgroups to
+// fill the GPU the rows are split between `splits` workgroups, whose
+// partial channel ranges the second kernel combines; otherwise the
+// workgroup writes the chunk's range itself.
+// A lane owns one 16-byte column = 8 channels of one head.  A wavefront
 // takes a segment of 512 channels of a row (rows of 1024 channels: two
 // wavefronts per row, each writing its own partial sum), or several narrow
-// rows.  Each wavefront loads kLagAhead rows (page-table entries first, then
-// the rows) before it uses any; with row segments the row, its page and its
-// address are wave-uniform (scalar).
+// rows; with row segments the row, its page and its address are
+// wave-uniform (scalar).  Each wavefront keeps a fixed number of rows in
+// flight: the loads of the next rows are issued as soon as a pair of rows
+// has been used, unconditionally (rows past its share are empty loads), so
+// that every use waits for its own rows only.
 //   Variance, one pass: the sum and the sum of squares over the head.  For
 //   the lag-normalised signals each channel is mapped to
 //   y = (x - mn) / (mx - mn + eps) - 1/2 (the shift keeps the sums of
 //   squares free of cancellation; a variance does not change under a
 //   shift); for the raw signals the packed bf16 words feed
 //   v_dot2_f32_bf16 directly (x0 + x1 and x0^2 + x1^2 in one instruction
-//   each, no unpacking).
+//   each, no unpacking).  Each lane's two sums of a row go to LDS; per
+//   batch of rows a transposed pass gives each lane one (row, head) pair,
+//   whose lanes' sums it adds in lane order, and the heads of a row are
+//   added with DPP row operations -- a few instructions per row instead of
+//   a cross-lane reduction of every row.
 //   Range (lag-normalised, not the first chunk): IEEE minimum / maximum
 //   over the rows -- a NaN propagates, as in a plain minimum over the chunk
-//   -- with three-input instructions over pairs of rows; the wavefronts'
-//   ranges are combined through LDS in a fixed tree.
+//   -- with three-input instructions over pairs of rows; the row slots'
+//   ranges meet in LDS, one slot each, and are reduced channel by channel
+//   in slot order.
 //   First chunk of a stream (lag-normalised): a first pass over the rows
 //   finds the chunk's range, the second computes the variances with it.
 // Per (row, plane, segment) the sum of its heads' variances goes to
@@ -46,17 +54,19 @@ namespace epikv {
 namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) int lds_int;
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of `width` lanes (2..32); every lane of a group
+// Sum over aligned groups of `width` lanes (1..64); every lane of a group
 // ends with the same bits (each step adds two values that the partner lane
 // adds in the other order).  Within a row of 16 lanes: DPP moves (quad
-// permutes, half-row mirror, rotations); across rows: a lane shuffle.
+// permutes, half-row mirror, rotations); across rows: lane shuffles.
 __device__ __forceinline__ float group_sum(float v, int width) {
+  if (width <= 1) return v;
   if (width == 2) return v + dpp<0xB1>(v);  // quad_perm [1,0,3,2]
   if (width == 4) {
     v += dpp<0xB1>(v);
@@ -71,19 +81,52 @@ __device__ __forceinline__ float group_sum(float v, int width) {
   v += dpp<0x124>(v);    // row_ror:4
   v += dpp<0x122>(v);    // row_ror:2
   v += dpp<0x121>(v);    // row_ror:1
-  if (width == 32) v += __shfl_xor(v, 16, 64);
+  if (width >= 32) v += __shfl_xor(v, 16, 64);
+  if (width == 64) v += __shfl_xor(v, 32, 64);
   return v;
 }
 
-// One 16-byte column of a row whose address is wave-uniform: a buffer
-// resource made for the row (scalar registers) and the lane's byte offset
-// as the only vector operand, so a row costs no vector address arithmetic.
-// The resource spans the row alone (offsets past it would read 0).
-// Non-temporal: each byte is read once.
-__device__ __forceinline__ u32x4 ld_row_nt(const char* row, uint32_t off, int row_bytes) {
+// Order of one wavefront's LDS accesses by its own lanes: the hardware
+// keeps them in issue order, the compiler must not move them across this.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Transposed head reduction (rows spanning whole wavefronts): each lane's
+// sum and sum of squares over its channels of a row go to LDS, the rows in
+// flight of kRedRowWords per wavefront; the padding after every 8 lanes
+// makes the transposed reads (8 lanes apart) hit distinct banks.
+__device__ __forceinline__ int red_word(int lane) { return (lane >> 3) * 20 + (lane & 7) * 2; }
+
+// NW consecutive 32-bit words (2 * NW bf16 channels, NW a multiple of 4)
+// of a row whose address is wave-uniform: a buffer resource made for the
+// row (scalar registers) and the lane's byte offset as the only vector
+// operand, so a row costs no vector address arithmetic.  The resource
+// spans the row alone; a missing row gets an empty resource, whose loads
+// return 0 without a memory access.  Non-temporal: each byte is read once.
+template <int NW>
+__device__ __forceinline__ void ld_row_nt(const char* row, uint32_t off, int n_bytes,
+                                          uint32_t (&w)[NW]) {
   const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, row_bytes, kBufferRsrcWord3);
-  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kBufferNonTemporal);
+      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, n_bytes, kBufferRsrcWord3);
+#pragma unroll
+  for (int c = 0; c < NW / 4; ++c) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * c, 0, kBufferNonTemporal);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[4 * c + k] = v[k];
+  }
+}
+// The same through a per-lane address (rows narrower than a wavefront).
+template <int NW>
+__device__ __forceinline__ void ld_lane_nt(const char* p, uint32_t (&w)[NW]) {
+#pragma unroll
+  for (int c = 0; c < NW / 4; ++c) {
+    const u32x4 v = ld_stream(p + 16 * c);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[4 * c + k] = v[k];
+  }
 }
 
 __device__ __forceinline__ float nan_min(float a, float b) {
@@ -93,21 +136,24 @@ __device__ __forceinline__ float nan_max(float a, float b) {
   return __builtin_elementwise_maximum(a, b);
 }
 
-// LAG: lag-normalised signal.  WIDE: rows of at least 512 channels, split
-// into segments of 64 lanes x CPL 16-byte columns (8 * CPL channels per
-// lane), one segment per wavefront, so the row, its page and its address
-// are wave-uniform; narrower rows are shared by the lanes of one
-// wavefront, 64 / row_vec rows at a time (CPL = 1).  The raw signals take
-// two columns per lane for rows of 1024 channels or more, which halves the
-// per-row work (cross-lane sums, addressing) per channel; the
-// lag-normalised form keeps one (its per-channel range and normalisation
-// would not fit 128 registers with two).
-template <bool LAG, bool WIDE, int CPL>
-__global__ __launch_bounds__(kLagThreads) __attribute__((amdgpu_waves_per_eu(4)))
-void k_score_lagkv(ScoreLagArgs a) {
-  constexpr int NCH = 8 * CPL;  // channels per lane
-  constexpr int AH = kLagAhead;  // rows per batch
-  static_assert(!(LAG && CPL > 1), "the lag-normalised form takes one column per lane");
+// LAG: lag-normalised signal.  NW: words (2 * NW channels) per lane.
+// WIDE: rows of at least 64 lanes, split into segments of 64 lanes, one
+// segment per wavefront, so the row, its page and its address are
+// wave-uniform; narrower rows are shared by the lanes of one wavefront,
+// 64 / (lanes per row) rows at a time.  WAVES: wavefronts per workgroup;
+// AH: rows each keeps in flight.  The lag-normalised signals carry four
+// registers of state per channel (the previous range's minimum and
+// scale, the running minimum and maximum): 512-thread workgroups of up
+// to 128 registers per lane with 8 rows in flight.  The raw signals carry
+// none: 1024-thread workgroups within 64 registers (two per CU), 4 rows in
+// flight.
+template <bool LAG, bool WIDE, int NW>
+__global__ __launch_bounds__(lagkv_threads(LAG))
+__attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArgs a) {
+  constexpr int NCH = 2 * NW;               // channels per lane
+  constexpr int WAVES = lagkv_waves(LAG);   // wavefronts per workgroup
+  constexpr int NT = WAVES * 64;
+  constexpr int AH = lagkv_ahead(LAG);      // rows in flight per wavefront
   extern __shared__ float lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -118,16 +164,16 @@ void k_score_lagkv(ScoreLagArgs a) {
   const int layer = a.two ? p >> 1 : p;
   const int kv = a.two ? (p & 1) : a.kv0;
   const int HD = a.H * a.d;
-  const int row_vec = HD >> 3;                    // 16-byte columns per row
-  const int segs = WIDE ? row_vec / (64 * CPL) : 1;  // wavefronts per row
-  const int lpr = WIDE ? 64 : row_vec;            // lanes per row segment
-  const int rpw = WIDE ? 1 : 64 / row_vec;        // rows per wavefront
-  const int seg = WIDE ? wave % segs : 0;         // this wavefront's segment
-  const int slot = WIDE ? wave / segs : wave;     // its row slot in the workgroup
-  const int rw = WIDE ? 0 : lane / lpr;           // this lane's row within the wavefront's
-  const int li = lane - rw * lpr;                 // lane within the segment
-  const int col = seg * 64 + li;                  // this lane's group of CPL columns
-  const int gw = a.d / NCH;                       // lanes per head
+  const int row_lanes = HD / NCH;                   // lanes per row
+  const int segs = WIDE ? row_lanes / 64 : 1;       // wavefronts per row
+  const int lpr = WIDE ? 64 : row_lanes;            // lanes per row segment
+  const int rpw = WIDE ? 1 : 64 / row_lanes;        // rows per wavefront
+  const int seg = WIDE ? wave % segs : 0;           // this wavefront's segment
+  const int slot = WIDE ? wave / segs : wave;       // its row slot in the workgroup
+  const int rw = WIDE ? 0 : lane / lpr;             // this lane's row within the wavefront's
+  const int li = lane - rw * lpr;                   // lane within the segment
+  const int col = seg * 64 + li;                    // this lane's group of NCH channels
+  const int gw = a.d / NCH;                         // lanes per head
   const int row_bytes = HD * 2;
 
   const int N = a.n_cached[b];
@@ -152,7 +198,7 @@ void k_score_lagkv(ScoreLagArgs a) {
     r_lo = min(a.C, sp * per);
     r_hi = min(a.C, r_lo + per);
   }
-  const int slots = kLagWaves / segs;                     // row slots of the workgroup
+  const int slots = WAVES / segs;                         // row slots of the workgroup
   // Each row slot walks its own contiguous block of the share's rows, rpw
   // rows per sweep (narrow rows: one per lane group), so consecutive rows
   // of a wavefront mostly share a page.
@@ -170,29 +216,31 @@ void k_score_lagkv(ScoreLagArgs a) {
   const int pg0 = any_rows ? page_index(start + r_lo) : 0;
   const int n_pg = any_rows ? page_index(start + r_hi - 1) - pg0 + 1 : 0;
   const bool cached = n_pg <= kLagPtCache;
-  int* lpt = reinterpret_cast<int*>(lds + (LAG ? lagkv_tree_floats(a.H, a.d) : 0));
+  float* red = lds + (LAG ? lagkv_range_floats(a.H, a.d) : 0);
+  int* lpt = reinterpret_cast<int*>(red + (WIDE ? WAVES * AH * kRedRowWords : 0));
   if (cached)
-    for (int i = tid; i < n_pg; i += kLagThreads) lpt[i] = pt[pg0 + i];
+    for (int i = tid; i < n_pg; i += NT) lpt[i] = pt[pg0 + i];
   __syncthreads();
   // The plane's base and this lane's column: a row address is the base
   // plus a wave-uniform row offset (row segments), to which the lane's
   // column is added by the load itself.
   const char* pbase = a.base + (int64_t)layer * a.s_layer + (int64_t)kv * a.s_kv;
-  const int loff = col * 16 * CPL;
+  const int loff = col * 4 * NW;
   // Byte offset (in the plane) of chunk row r, -1 if the row is not this
   // wavefront's or its page is out of range.
   auto row_off = [&](int r) -> int64_t {
     if (!seq_ok || r >= s_hi) return -1;
     const int pos = start + r;
     const int pidx = page_index(pos);
-    const int pg = cached ? lpt[pidx - pg0] : pt[pidx];
+    // (an LDS-typed read: a generic load of either table would make the
+    // compiler wait for every row load in flight)
+    const int pg = cached ? ((const lds_int*)lpt)[pidx - pg0] : pt[pidx];
     if (pg < 0 || pg >= a.n_pages) return -1;
     return (int64_t)pg * a.s_page + (int64_t)(pos - pidx * a.page_size) * row_bytes;
   };
   // Row segments: lane i keeps the offset of row tb + i of the wavefront's
   // block (a table refilled every 64 rows), and a row's offset is read
-  // from it with readlane -- no memory round trip per row, and (the table
-  // being computed, not loaded) no wait for the rows in flight.
+  // from it with readlane -- no memory round trip per row.
   int tb = -(1 << 30);
   uint32_t t_lo = 0, t_hi = 0;
   auto row_addr = [&](int r, bool& ok) -> const char* {
@@ -213,19 +261,17 @@ void k_score_lagkv(ScoreLagArgs a) {
     ok = off >= 0;
     return ok ? pbase + off : pbase;
   };
-  // Load the rows of sweeps it0 .. it0 + kLagAhead - 1; ok[u]: row present.
-  // Every load is issued (a missing row reads the plane's first row and is
-  // ignored), so the loads are straight-line code and the compiler can
-  // wait for each batch alone rather than for every load in flight.
-  auto load_rows = [&](int it0, u32x4 (&raw)[AH][CPL], bool (&ok)[AH]) {
-#pragma unroll
-    for (int u = 0; u < AH; ++u) {
-      const char* q = row_addr(row_of(it0 + u), ok[u]);
-#pragma unroll
-      for (int c = 0; c < CPL; ++c)
-        raw[u][c] = WIDE ? ld_row_nt(q, (uint32_t)(loff + 16 * c), row_bytes)
-                         : ld_stream(q + loff + 16 * c);
-    }
+  // Row r's words for this lane; every load is issued, also past the
+  // wavefront's rows (row segments: a missing row's loads are empty and
+  // read 0; narrow rows: it reads the plane's first row and is ignored),
+  // so that the loads in flight are the same on every path: the compiler
+  // then waits for each row alone, not for the rows in flight behind it.
+  auto load_row = [&](int r, uint32_t (&w)[NW], bool& ok) {
+    const char* q = row_addr(r, ok);
+    if (WIDE)
+      ld_row_nt<NW>(q, (uint32_t)loff, ok ? row_bytes : 0, w);
+    else
+      ld_lane_nt<NW>(q + loff, w);
   };
 
   float cmn[NCH], cmx[NCH];  // this lane's channels' range over its rows
@@ -234,64 +280,40 @@ void k_score_lagkv(ScoreLagArgs a) {
     cmn[e] = __builtin_huge_valf();
     cmx[e] = -__builtin_huge_valf();
   }
-  auto unpack = [](const u32x4 (&w)[CPL], float (&x)[NCH]) {
-#pragma unroll
-    for (int c = 0; c < CPL; ++c)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        x[c * 8 + 2 * k] = bf16_lo(w[c][k]);
-        x[c * 8 + 2 * k + 1] = bf16_hi(w[c][k]);
-      }
-  };
-  auto track = [&](const float (&x)[NCH]) {
-#pragma unroll
-    for (int e = 0; e < NCH; ++e) {
-      cmn[e] = nan_min(cmn[e], x[e]);
-      cmx[e] = nan_max(cmx[e], x[e]);
-    }
-  };
-  // Combine the range over the workgroup's row slots (and the rows of one
-  // wavefront) in a fixed tree through LDS, slots of [2][H*d] floats; the
-  // partial of slot 0 ends with the result.  With `bcast` every lane then
-  // reads it.
+  // The chunk's range over the workgroup's rows: every row slot (and,
+  // narrow rows, row of a wavefront) leaves its partial range in its own
+  // LDS slot of [2][H*d] floats (minima, then maxima); after a barrier
+  // thread t reduces channels t, t + NT, ... over the slots in slot order
+  // and writes the result to `dst` (the state, or this share's part for
+  // the second kernel) and, with `keep`, back into slot 0.
   const int n_part = slots * rpw;
   const int vid = slot * rpw + rw;
-  auto combine = [&](bool bcast) {
-    for (int s = n_part / 2; s >= 1; s >>= 1) {
-      if (vid >= s && vid < 2 * s) {
-        float* sl = lds + (int64_t)(vid - s) * 2 * HD + col * NCH;
+  auto deposit = [&]() {
+    float* sl = lds + (int64_t)vid * 2 * HD + col * NCH;
 #pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-          sl[e] = cmn[e];
-          sl[HD + e] = cmx[e];
-        }
-      }
-      __syncthreads();
-      if (vid < s) {
-        const float* sl = lds + (int64_t)vid * 2 * HD + col * NCH;
-#pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-          cmn[e] = nan_min(cmn[e], sl[e]);
-          cmx[e] = nan_max(cmx[e], sl[HD + e]);
-        }
-      }
-      __syncthreads();
+    for (int e = 0; e < NCH; ++e) {
+      sl[e] = cmn[e];
+      sl[HD + e] = cmx[e];
     }
-    if (bcast) {
-      if (vid == 0) {
-#pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-          lds[col * NCH + e] = cmn[e];
-          lds[HD + col * NCH + e] = cmx[e];
-        }
+  };
+  const int64_t plane_off = (((int64_t)b * a.L + layer) * 2 + kv) * HD;
+  auto combine = [&](bool keep) {
+    __syncthreads();
+    float* dst = a.splits == 1 ? a.range_out : a.prange + (int64_t)sp * 2 * half;
+    for (int i = tid; i < 2 * HD; i += NT) {
+      float v = lds[i];
+      for (int k = 1; k < n_part; ++k) {
+        const float o = lds[(int64_t)k * 2 * HD + i];
+        v = i < HD ? nan_min(v, o) : nan_max(v, o);
       }
-      __syncthreads();
-#pragma unroll
-      for (int e = 0; e < NCH; ++e) {
-        cmn[e] = lds[col * NCH + e];
-        cmx[e] = lds[HD + col * NCH + e];
+      dst[(i < HD ? 0 : half - HD) + plane_off + i] = v;
+      if (keep) lds[i] = v;
+      if (a.splits == 1 && !a.two) {
+        // a one-tensor signal carries no range for the other tensor
+        a.range_out[(i < HD ? 0 : half - HD) + plane_off + (int64_t)(1 - 2 * kv) * HD + i] = 0.f;
       }
     }
+    __syncthreads();
   };
 
   // y = (x - mn) * sc - 1/2: the normalisation (shifted by -1/2) of each
@@ -302,23 +324,26 @@ void k_score_lagkv(ScoreLagArgs a) {
   if (LAG) {
     if (fresh) {
       // first pass: the chunk's own range
-      for (int it0 = 0; it0 < sweeps; it0 += AH) {
-        u32x4 raw[AH][CPL];
-        bool ok[AH];
-        load_rows(it0, raw, ok);
+      for (int it = 0; it < sweeps; ++it) {
+        uint32_t w[NW];
+        bool ok;
+        load_row(row_of(it), w, ok);
+        if (ok)
 #pragma unroll
-        for (int u = 0; u < AH; ++u) {
-          float x[NCH];
-          unpack(raw[u], x);
-          if (ok[u]) track(x);
-        }
+          for (int k = 0; k < NW; ++k) {
+            cmn[2 * k] = nan_min(cmn[2 * k], bf16_lo(w[k]));
+            cmx[2 * k] = nan_max(cmx[2 * k], bf16_lo(w[k]));
+            cmn[2 * k + 1] = nan_min(cmn[2 * k + 1], bf16_hi(w[k]));
+            cmx[2 * k + 1] = nan_max(cmx[2 * k + 1], bf16_hi(w[k]));
+          }
       }
+      deposit();
       combine(true);
     }
 #pragma unroll
     for (int e = 0; e < NCH; ++e) {
-      const float mn = fresh ? cmn[e] : a.range_in[rbase + e];
-      const float mx = fresh ? cmx[e] : a.range_in[half + rbase + e];
+      const float mn = fresh ? lds[col * NCH + e] : a.range_in[rbase + e];
+      const float mx = fresh ? lds[HD + col * NCH + e] : a.range_in[half + rbase + e];
       mnv[e] = mn;
       sc[e] = 1.0f / (mx - mn + a.eps);
     }
@@ -326,153 +351,169 @@ void k_score_lagkv(ScoreLagArgs a) {
 
   const float inv_d = 1.0f / (float)a.d;
   const bf16x2 one2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1, 1)
-  // Variance of this lane's head for one row from the sum and the sum of
-  // squares of its values (lag-normalised: y = (x - mn) * sc - 1/2 per
-  // channel, the variance being that of x~): every lane of the wavefront runs it (the group sums see every
-  // lane of a group).  A missing row is computed like any other and its
+  // Variance of a head from the sum and the sum of squares of its values
+  // (lag-normalised: y = (x - mn) * sc - 1/2 per channel, the variance
+  // being that of x~).  A missing row is computed like any other and its
   // result dropped at the write: a load whose value might go unused forces
   // a wait for every load in flight before its register is reused.
-  auto finish_var = [&](float s, float q) -> float {
-    s = group_sum(s, gw);
-    q = group_sum(q, gw);
+  auto head_var = [&](float s, float q) -> float {
     const float mu = s * inv_d;
     return fmaf(-mu, mu, q * inv_d);
   };
   // raw: x0 + x1 and x0^2 + x1^2 of each packed pair in one instruction
-  auto var_raw = [&](const u32x4 (&w)[CPL]) -> float {
-    float s = 0.f, q = 0.f;
+  auto sums_raw = [&](const uint32_t (&w)[NW], float& s, float& q) {
+    s = 0.f;
+    q = 0.f;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c)
+    for (int k = 0; k < NW; ++k) {
+      const bf16x2 x = __builtin_bit_cast(bf16x2, w[k]);
+      s = __builtin_amdgcn_fdot2_f32_bf16(x, one2, s, false);
+      q = __builtin_amdgcn_fdot2_f32_bf16(x, x, q, false);
+    }
+  };
+
+  // Transposed reduction of a batch of AH rows (row segments): lane l
+  // takes the (row, head) pair l / lpp of the batch -- lpp lanes per pair
+  // when a head spans more lanes than the batch has rows -- adds m =
+  // gw / lpp lanes' partials in lane order, the pair's lanes combine
+  // theirs, and the heads of a row (rg adjacent lanes) are summed.
+  const int hs = 64 / gw;                       // heads per row segment
+  const int lpp = gw > AH ? gw / AH : 1;
+  const int m = gw / lpp;
+  const int ppp = 64 / lpp;                     // pairs per pass
+  const int passes = WIDE ? AH * hs / ppp : 0;
+  const int rg = hs * lpp;
+  float* red_w = red + wave * AH * kRedRowWords;
+  auto put = [&](int u, float s, float q) {
+    *reinterpret_cast<float2*>(red_w + u * kRedRowWords + red_word(lane)) = make_float2(s, q);
+  };
+  auto reduce_batch = [&](int it0, uint32_t okm) {
+    wave_sync();
+    for (int ps = 0; ps < passes; ++ps) {
+      const int P = ps * ppp + lane / lpp;
+      const int j = lane & (lpp - 1);
+      const int u = P / hs;
+      const int h = P - u * hs;
+      const float* src = red_w + u * kRedRowWords;
+      const int l0 = h * gw + j * m;
+      float S = 0.f, Q = 0.f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        // (through a scalar: a bit cast of the vector element itself
-        // reads element 0)
-        const uint32_t wk = w[c][k];
-        const bf16x2 x = __builtin_bit_cast(bf16x2, wk);
-        s = __builtin_amdgcn_fdot2_f32_bf16(x, one2, s, false);
-        q = __builtin_amdgcn_fdot2_f32_bf16(x, x, q, false);
-      }
-    return finish_var(s, q);
+      for (int i = 0; i < AH; ++i)
+        if (i < m) {
+          const float2 v = *reinterpret_cast<const float2*>(src + red_word(l0 + i));
+          S += v.x;
+          Q += v.y;
+        }
+      S = group_sum(S, lpp);
+      Q = group_sum(Q, lpp);
+      const float rs = group_sum(j == 0 ? head_var(S, Q) : 0.f, rg);
+      const int r = s_lo + it0 + u;
+      if ((lane & (rg - 1)) == 0 && r < s_hi) part[r] = (okm >> u) & 1 ? rs : 0.f;
+    }
+    wave_sync();
   };
 
   const bool track_range = LAG && !fresh;
-  // Rows of sweeps it0 .. it0 + kLagAhead - 1: the range, then each head's
-  // variance, written by the head's first lane (rows past the share are
-  // not written).
-  auto process = [&](int it0, const u32x4 (&raw)[AH][CPL], const bool (&ok)[AH]) {
-    float v[AH];
+  // Rows u and u + 1 of the batch at sweep it0: the range, then each
+  // lane's sum and sum of squares (row segments: into LDS for the batch's
+  // transposed reduction; narrow rows: each head's variance, the row's
+  // heads added with lane shuffles in lane order and written by the row's
+  // first lane).  Rows past the share are not written.
+  auto process_pair = [&](int it0, int u, const uint32_t (&wa)[NW], const uint32_t (&wb)[NW],
+                          bool oka, bool okb) {
+    float sa = 0.f, qa = 0.f, sb = 0.f, qb = 0.f;
     if (LAG) {
-      // rows in pairs, one packed word at a time: each value unpacked
-      // once, for the range and the sums
+      // one packed word at a time: each value unpacked once, for the
+      // range and the sums
+      auto sums = [&](float xa, float xb, int e) {
+        const float ya = fmaf(xa - mnv[e], sc[e], -0.5f);
+        const float yb = fmaf(xb - mnv[e], sc[e], -0.5f);
+        sa += ya;
+        qa = fmaf(ya, ya, qa);
+        sb += yb;
+        qb = fmaf(yb, yb, qb);
+      };
+      if (track_range && oka && okb) {
+        // both rows present: three-input minimum / maximum
 #pragma unroll
-      for (int u = 0; u < AH; u += 2) {
-        float sa = 0.f, qa = 0.f, sb = 0.f, qb = 0.f;
-        auto sums = [&](float xa, float xb, int e) {
-          const float ya = fmaf(xa - mnv[e], sc[e], -0.5f);
-          const float yb = fmaf(xb - mnv[e], sc[e], -0.5f);
-          sa += ya;
-          qa = fmaf(ya, ya, qa);
-          sb += yb;
-          qb = fmaf(yb, yb, qb);
-        };
-        if (track_range && WIDE && ok[u] && ok[u + 1]) {
-#pragma unroll
-          for (int c = 0; c < CPL; ++c)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              const int e = c * 8 + 2 * k;
-              const float a0 = bf16_lo(raw[u][c][k]), a1 = bf16_hi(raw[u][c][k]);
-              const float b0 = bf16_lo(raw[u + 1][c][k]), b1 = bf16_hi(raw[u + 1][c][k]);
-              cmn[e] = nan_min(cmn[e], nan_min(a0, b0));
-              cmx[e] = nan_max(cmx[e], nan_max(a0, b0));
-              cmn[e + 1] = nan_min(cmn[e + 1], nan_min(a1, b1));
-              cmx[e + 1] = nan_max(cmx[e + 1], nan_max(a1, b1));
-              sums(a0, b0, e);
-              sums(a1, b1, e + 1);
-            }
-        } else {
-#pragma unroll
-          for (int c = 0; c < CPL; ++c)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              const int e = c * 8 + 2 * k;
-              const float a0 = bf16_lo(raw[u][c][k]), a1 = bf16_hi(raw[u][c][k]);
-              const float b0 = bf16_lo(raw[u + 1][c][k]), b1 = bf16_hi(raw[u + 1][c][k]);
-              if (track_range && ok[u]) {
-                cmn[e] = nan_min(cmn[e], a0);
-                cmx[e] = nan_max(cmx[e], a0);
-                cmn[e + 1] = nan_min(cmn[e + 1], a1);
-                cmx[e + 1] = nan_max(cmx[e + 1], a1);
-              }
-              if (track_range && ok[u + 1]) {
-                cmn[e] = nan_min(cmn[e], b0);
-                cmx[e] = nan_max(cmx[e], b0);
-                cmn[e + 1] = nan_min(cmn[e + 1], b1);
-                cmx[e + 1] = nan_max(cmx[e + 1], b1);
-              }
-              sums(a0, b0, e);
-              sums(a1, b1, e + 1);
-            }
+        for (int k = 0; k < NW; ++k) {
+          const int e = 2 * k;
+          const float a0 = bf16_lo(wa[k]), a1 = bf16_hi(wa[k]);
+          const float b0 = bf16_lo(wb[k]), b1 = bf16_hi(wb[k]);
+          cmn[e] = nan_min(cmn[e], nan_min(a0, b0));
+          cmx[e] = nan_max(cmx[e], nan_max(a0, b0));
+          cmn[e + 1] = nan_min(cmn[e + 1], nan_min(a1, b1));
+          cmx[e + 1] = nan_max(cmx[e + 1], nan_max(a1, b1));
+          sums(a0, b0, e);
+          sums(a1, b1, e + 1);
         }
-        v[u] = finish_var(sa, qa);
-        v[u + 1] = finish_var(sb, qb);
+      } else {
+#pragma unroll
+        for (int k = 0; k < NW; ++k) {
+          const int e = 2 * k;
+          const float a0 = bf16_lo(wa[k]), a1 = bf16_hi(wa[k]);
+          const float b0 = bf16_lo(wb[k]), b1 = bf16_hi(wb[k]);
+          if (track_range && oka) {
+            cmn[e] = nan_min(cmn[e], a0);
+            cmx[e] = nan_max(cmx[e], a0);
+            cmn[e + 1] = nan_min(cmn[e + 1], a1);
+            cmx[e + 1] = nan_max(cmx[e + 1], a1);
+          }
+          if (track_range && okb) {
+            cmn[e] = nan_min(cmn[e], b0);
+            cmx[e] = nan_max(cmx[e], b0);
+            cmn[e + 1] = nan_min(cmn[e + 1], b1);
+            cmx[e + 1] = nan_max(cmx[e + 1], b1);
+          }
+          sums(a0, b0, e);
+          sums(a1, b1, e + 1);
+        }
       }
     } else {
-#pragma unroll
-      for (int u = 0; u < AH; ++u) v[u] = var_raw(raw[u]);
+      sums_raw(wa, sa, qa);
+      sums_raw(wb, sb, qb);
     }
-#pragma unroll
-    for (int u = 0; u < AH; ++u) {
-      const int r = row_of(it0 + u);
-      // the heads of the segment summed in lane order: with row segments
-      // one lane per head group is read into a scalar, narrow rows add
-      // their groups with lane shuffles
-      float sum;
-      if (WIDE) {
-        sum = 0.f;
-        for (int g = 0; g < 64; g += gw)
-          sum += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[u]), g));
-      } else {
-        sum = v[u];
-        for (int off = gw; off < lpr; off <<= 1) sum += __shfl_xor(sum, off, 64);
-      }
-      if (li == 0 && r < s_hi) part[r] = ok[u] ? sum : 0.f;
+    if (WIDE) {
+      put(u, sa, qa);
+      put(u + 1, sb, qb);
+      return;
     }
+    float va = head_var(group_sum(sa, gw), group_sum(qa, gw));
+    float vb = head_var(group_sum(sb, gw), group_sum(qb, gw));
+    for (int off = gw; off < lpr; off <<= 1) {
+      va += __shfl_xor(va, off, 64);
+      vb += __shfl_xor(vb, off, 64);
+    }
+    const int r = row_of(it0 + u);
+    if (li == 0 && r < s_hi) part[r] = oka ? va : 0.f;
+    if (li == 0 && r + rpw < s_hi) part[r + rpw] = okb ? vb : 0.f;
   };
-  // Software pipelined over two buffers: the next batch of rows is in
-  // flight while this one is used.
-  u32x4 ra[AH][CPL], rb[AH][CPL];
-  bool oa[AH], ob[AH];
-  if (sweeps > 0) load_rows(0, ra, oa);
-  for (int it0 = 0; it0 < sweeps; it0 += 2 * AH) {
-    if (it0 + AH < sweeps) load_rows(it0 + AH, rb, ob);
-    process(it0, ra, oa);
-    if (it0 + AH >= sweeps) break;
-    if (it0 + 2 * AH < sweeps) load_rows(it0 + 2 * AH, ra, oa);
-    process(it0 + AH, rb, ob);
+  // Rolling pipeline over AH rows in flight: as soon as a pair of rows is
+  // used its registers receive the pair AH rows on.  Every load is
+  // unconditional, so the loads in flight are the same on every path and
+  // each use waits for its own pair only.
+  if (sweeps > 0) {
+    uint32_t raw[AH][NW];
+    bool ok[AH];
+#pragma unroll
+    for (int u = 0; u < AH; ++u) load_row(row_of(u), raw[u], ok[u]);
+    for (int it0 = 0;; it0 += AH) {
+      uint32_t okm = 0;
+#pragma unroll
+      for (int u = 0; u < AH; u += 2) {
+        process_pair(it0, u, raw[u], raw[u + 1], ok[u], ok[u + 1]);
+        okm |= (ok[u] ? 1u << u : 0u) | (ok[u + 1] ? 2u << u : 0u);
+        load_row(row_of(it0 + AH + u), raw[u], ok[u]);
+        load_row(row_of(it0 + AH + u + 1), raw[u + 1], ok[u + 1]);
+      }
+      if (WIDE) reduce_batch(it0, okm);
+      if (it0 + AH >= sweeps) break;
+    }
   }
 
-  if (LAG) {
-    if (!fresh) combine(false);
-    if (vid == 0) {
-      // the chunk's range: straight into the state when one workgroup saw
-      // every row, else this share's part for the second kernel
-      float* dst = a.splits == 1 ? a.range_out : a.prange + (int64_t)sp * 2 * half;
-#pragma unroll
-      for (int e = 0; e < NCH; ++e) {
-        dst[rbase + e] = cmn[e];
-        dst[half + rbase + e] = cmx[e];
-      }
-      if (a.splits == 1 && !a.two) {
-        // a one-tensor signal carries no range for the other tensor
-        const int64_t other = rbase + (int64_t)(1 - 2 * kv) * HD;
-#pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-          a.range_out[other + e] = 0.f;
-          a.range_out[half + other + e] = 0.f;
-        }
-      }
-    }
+  if (LAG && !fresh) {
+    deposit();
+    combine(false);
   }
 }
 
@@ -528,29 +569,30 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
   a.range_out[half + o] = hi;
 }
 
-template <bool WIDE, int CPL>
+template <bool LAG, bool WIDE, int NW>
 hipError_t launch_lag(const ScoreLagArgs& a, hipStream_t s) {
   const dim3 grid(a.n_planes, a.B, a.splits);
   const size_t lds = lagkv_lds_bytes(a.H, a.d, a.lag);
-  if (CPL == 1 && a.lag)
-    hipLaunchKernelGGL((k_score_lagkv<true, WIDE, 1>), grid, dim3(kLagThreads), lds, s, a);
-  else
-    hipLaunchKernelGGL((k_score_lagkv<false, WIDE, CPL>), grid, dim3(kLagThreads), lds, s, a);
+  hipLaunchKernelGGL((k_score_lagkv<LAG, WIDE, NW>), grid, dim3(lagkv_threads(LAG)), lds, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 size_t lagkv_lds_bytes(int H, int d, bool lag) {
-  return (lag ? lagkv_tree_floats(H, d) * sizeof(float) : 0) + kLagPtCache * sizeof(int);
+  return (lag ? lagkv_range_floats(H, d) * sizeof(float) : 0) +
+         (lagkv_wide(H, d, lag)
+              ? (size_t)lagkv_waves(lag) * lagkv_ahead(lag) * kRedRowWords * sizeof(float)
+              : 0) +
+         kLagPtCache * sizeof(int);
 }
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
-  const int cpl = lagkv_cpl(a.H, a.d, a.lag);
-  const int row_vec = a.H * a.d / 8;
-  const hipError_t e = cpl == 2        ? launch_lag<true, 2>(a, s)
-                       : row_vec >= 64 ? launch_lag<true, 1>(a, s)
-                                       : launch_lag<false, 1>(a, s);
+  const bool wide = lagkv_wide(a.H, a.d, a.lag);
+  const hipError_t e = a.lag ? (wide ? launch_lag<true, true, kLagWords>(a, s)
+                                     : launch_lag<true, false, kLagWords>(a, s))
+                             : (wide ? launch_lag<false, true, kLagWords>(a, s)
+                                     : launch_lag<false, false, kLagWords>(a, s));
   if (e != hipSuccess) return e;
   const int tok_blocks = (r.C + kRedTok - 1) / kRedTok;
   const int rng_blocks = r.lag && r.splits > 1 ? (r.n_chan + kScoreThreads - 1) / kScoreThreads : 0;
