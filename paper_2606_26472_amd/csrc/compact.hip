@@ -12,11 +12,12 @@
 //            a plain copy does even when the allocator scattered the
 //            destination pages (measured on MI355X: 5.2 -> 6.2 TB/s for
 //            randomly placed pages; a cache rebuilt into one run of pages
-//            per sequence is already in that order).  Page ids of the used
-//            pages are marked in an LDS bitmap over their range, and a page's
-//            rank is the number of marked ids below it.  A range too wide
-//            for the bitmap, or a page id used twice, keeps the logical
-//            order (sequence, page).
+//            per sequence is already in that order).  When the used ids
+//            already rise in logical order the ranks follow from two prefix
+//            counts; otherwise the used ids are marked in an LDS bitmap over
+//            their range, and a page's rank is the number of marked ids
+//            below it.  A range too wide for the bitmap, or a page id used
+//            twice, keeps the logical order (sequence, page).
 //   resolve  one thread per slot of the budget's pages turns keep_idx and
 //            the two page tables into the byte offsets of the source and
 //            destination rows inside a plane, a 16-byte record written at
@@ -39,14 +40,36 @@ namespace {
 constexpr int kOrderThreads = 1024;
 constexpr int kOrderWords = 16384;  // bitmap words: page ids spanning up to 512 Ki
 
+// Exclusive prefix sum of one value per thread over the workgroup, in
+// thread order; *total gets the sum.  (wsum: kOrderThreads / 64 words.)
+__device__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t t = __shfl_up(x, off, 64);
+    if (lane >= off) x += t;
+  }
+  __syncthreads();
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+  for (int w = 0; w < kOrderThreads / 64; ++w) {
+    base += w < wave ? wsum[w] : 0u;
+    tot += wsum[w];
+  }
+  *total = tot;
+  return base + x - v;
+}
+
 __global__ __launch_bounds__(kOrderThreads) void k_compact_order(CompactArgs a) {
   __shared__ uint32_t bits[kOrderWords];
-  __shared__ uint32_t pre[kOrderThreads];  // per-thread prefix (bitmap chunks, then invalid entries)
+  __shared__ uint32_t pre[kOrderThreads];  // per-thread prefix of the bitmap chunks
   __shared__ uint32_t wsum[kOrderThreads / 64];
-  __shared__ int s_lo, s_hi, s_logical;
+  __shared__ int s_lo, s_hi, s_logical, s_unsorted;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
   const int n_pg = a.n_pg;
   const int64_t N = (int64_t)a.B * n_pg;
   int32_t* rank = a.rank;
@@ -62,6 +85,63 @@ __global__ __launch_bounds__(kOrderThreads) void k_compact_order(CompactArgs a) 
     return (pg >= 0 && pg < a.d_npages) ? pg : -1;
   };
 
+  // Each thread takes a contiguous range of entries: its used and unused
+  // counts, and whether its used page ids rise strictly.
+  const int64_t per = (N + kOrderThreads - 1) / kOrderThreads;
+  const int64_t e0 = (int64_t)tid * per;
+  const int64_t e1 = min(N, e0 + per);
+  uint32_t n_use = 0, n_bad = 0;
+  int first = -1, last = -1;
+  bool rising = true;
+  for (int64_t e = e0; e < e1; ++e) {
+    const int pg = page_of(e);
+    if (pg < 0) {
+      ++n_bad;
+    } else {
+      if (last >= 0 && pg <= last) rising = false;
+      if (first < 0) first = pg;
+      last = pg;
+      ++n_use;
+    }
+  }
+  if (tid == 0) {
+    s_lo = INT32_MAX;
+    s_hi = -1;
+    s_logical = 0;
+    s_unsorted = 0;
+  }
+  uint32_t n_used, n_unused;
+  uint32_t used_before = block_exclusive_sum(n_use, wsum, &n_used);
+  uint32_t bad_before = block_exclusive_sum(n_bad, wsum, &n_unused);
+  // The used page ids rise strictly over all entries iff every thread's do
+  // and each thread's first exceeds the last of the threads before it.
+  {
+    int mx = last;  // inclusive prefix maximum of the threads' last ids
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int t = __shfl_up(mx, off, 64);
+      if (lane >= off) mx = max(mx, t);
+    }
+    __syncthreads();
+    if (lane == 63) wsum[tid >> 6] = (uint32_t)(mx + 1);
+    __syncthreads();
+    int before = __shfl_up(mx, 1, 64);
+    if (lane == 0) before = -1;
+    for (int w = 0; w < (tid >> 6); ++w) before = max(before, (int)wsum[w] - 1);
+    if (!rising || (first >= 0 && first <= before)) atomicOr(&s_unsorted, 1);
+    __syncthreads();
+  }
+
+  // Rising: a used page's rank (the number of used ids below it) is the
+  // number of used entries before it; the unused entries follow, in
+  // logical order.
+  if (!s_unsorted) {
+    for (int64_t e = e0; e < e1; ++e)
+      rank[e] = page_of(e) >= 0 ? (int32_t)used_before++ : (int32_t)(n_used + bad_before++);
+    return;
+  }
+
+  // Otherwise the ranks come from a bitmap of the used ids over their range.
   // 1. the range of the used page ids
   int lo = INT32_MAX, hi = -1;
   for (int64_t e = tid; e < N; e += kOrderThreads) {
@@ -76,12 +156,6 @@ __global__ __launch_bounds__(kOrderThreads) void k_compact_order(CompactArgs a) 
     lo = min(lo, __shfl_xor(lo, off, 64));
     hi = max(hi, __shfl_xor(hi, off, 64));
   }
-  if (tid == 0) {
-    s_lo = INT32_MAX;
-    s_hi = -1;
-    s_logical = 0;
-  }
-  __syncthreads();
   if (lane == 0) {
     atomicMin(&s_lo, lo);
     atomicMax(&s_hi, hi);
@@ -111,53 +185,17 @@ __global__ __launch_bounds__(kOrderThreads) void k_compact_order(CompactArgs a) 
   // 3. ranks: a used page's is the number of used ids below it; the
   //    unused entries follow, in logical order
   const int chunk = (words + kOrderThreads - 1) / kOrderThreads;  // bitmap words per thread
-  uint32_t n_used = 0;
   if (!logical) {
     uint32_t c = 0;
     for (int k = 0; k < chunk; ++k) {
       const int w = tid * chunk + k;
       if (w < words) c += __popc(bits[w]);
     }
-    // exclusive scan of the per-thread counts
-    uint32_t x = c;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t t = __shfl_up(x, off, 64);
-      if (lane >= off) x += t;
-    }
-    if (lane == 63) wsum[wave] = x;
-    __syncthreads();
-    uint32_t base = 0, tot = 0;
-    for (int w = 0; w < kOrderThreads / 64; ++w) {
-      base += w < wave ? wsum[w] : 0u;
-      tot += wsum[w];
-    }
-    pre[tid] = base + x - c;
-    n_used = tot;
+    uint32_t tot;
+    pre[tid] = block_exclusive_sum(c, wsum, &tot);
     __syncthreads();
   }
-  // invalid entries, counted in contiguous per-thread ranges of entries
-  const int64_t per = (N + kOrderThreads - 1) / kOrderThreads;
-  const int64_t e0 = (int64_t)tid * per;
-  uint32_t n_bad = 0;
-  if (!logical)
-    for (int64_t e = e0; e < min(N, e0 + per); ++e) n_bad += page_of(e) < 0 ? 1u : 0u;
-  uint32_t bad_before = 0;
-  {
-    uint32_t x = n_bad;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const uint32_t t = __shfl_up(x, off, 64);
-      if (lane >= off) x += t;
-    }
-    __syncthreads();  // (wsum is reused)
-    if (lane == 63) wsum[wave] = x;
-    __syncthreads();
-    uint32_t base = 0;
-    for (int w = 0; w < wave; ++w) base += wsum[w];
-    bad_before = base + x - n_bad;
-  }
-  for (int64_t e = e0; e < min(N, e0 + per); ++e) {
+  for (int64_t e = e0; e < e1; ++e) {
     int32_t r;
     if (logical) {
       r = (int32_t)e;

@@ -21,7 +21,9 @@
 //          past the end of this tile (their sources are >= their own slots).
 //          So one wavefront per column slice moves its bytes without any
 //          barrier or second copy, and different slices, planes and
-//          sequences touch disjoint bytes.
+//          sequences touch disjoint bytes.  With 1 KiB slices the walk is
+//          pipelined: the next tile's loads are in flight while this tile
+//          is stored (they read past every slot written so far).
 //
 // With page remapping (epikv_compact_remap) the check kernel also rewrites
 // the page table so that whole retained pages change places instead of being
@@ -372,6 +374,114 @@ __global__ __launch_bounds__(kCompactThreads) void k_inplace_move(InplaceArgs a)
   }
 }
 
+// The move for 1 KiB column slices (64 lanes per row, one row per
+// instruction), software pipelined: tile k + 1's loads are issued before
+// tile k's stores, and a tile's stores wait only for its own loads.  This
+// keeps the ordering argument: tile k + 1 reads positions at or past its
+// own slots, which lie past every slot tile k (or any earlier tile)
+// writes, and tile k's stores follow its loads.  Every load and store is
+// issued, a missing row or record through an empty buffer resource (its
+// loads read 0 without a memory access, its stores are dropped), so that
+// the operations in flight are the same on every path and each wait is
+// exactly for the tile it needs.
+// One (src, dst) record per lane for the rows of a tile: lane t < NI holds
+// the tile's row t (a lane past the walk's rows loads the first record
+// and is marked absent).
+template <int NI>
+struct WalkRecs {
+  int64_t s, d;
+  int in;
+};
+
+__device__ __forceinline__ void st_row_nt(char* row, uint32_t off, int n_bytes, u32x4 v) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, n_bytes, kBufferRsrcWord3);
+  __builtin_amdgcn_raw_buffer_store_b128(v, rs, off, 0, kBufferNonTemporal);
+}
+__device__ __forceinline__ u32x4 ld_row_nt(const char* row, uint32_t off, int n_bytes) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, n_bytes, kBufferRsrcWord3);
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kBufferNonTemporal);
+}
+
+template <int NI>
+__global__ __launch_bounds__(kCompactThreads) void k_inplace_walk(InplaceArgs a) {
+  static_assert(NI <= 64, "a tile's records fit one register per lane");
+  const int lane = threadIdx.x & 63;
+  // (the wavefront index made explicitly uniform, so that everything derived
+  // from it -- the walk's plane and slice, hence each row's buffer resource --
+  // lives in scalar registers)
+  const int64_t unit =
+      (int64_t)blockIdx.x * kCompactWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t per_seq = (int64_t)a.n_lk * a.n_slices;
+  const int b = (int)(unit / per_seq);
+  if (b >= a.B) return;
+  const int rem = (int)(unit - (int64_t)b * per_seq);
+  const int pl = rem / a.n_slices;
+  const int sl = rem - pl * a.n_slices;
+  const int h = a.info[2 * b];
+  const int nk = a.info[2 * b + 1];
+  if (h >= nk) return;
+  // this slice of a row: bytes [1024 sl, min(1024 sl + 1024, row_bytes))
+  char* base = a.pool + (int64_t)(pl >> 1) * a.s_layer + (int64_t)(pl & 1) * a.s_kv + 1024 * sl;
+  const int span = min(1024, a.row_bytes - 1024 * sl);
+  const uint32_t off = 16u * lane;
+  const int64_t* rec = a.offsets + 2 * (int64_t)b * a.K;
+  auto load_recs = [&](int j0, WalkRecs<NI>& r) {
+    const int t = j0 + lane;
+    r.in = lane < NI && t < nk;
+    const int tc = r.in ? t : h;
+    r.s = rec[2 * tc];
+    r.d = rec[2 * tc + 1];
+  };
+  // row i of a tile: its source (load) or destination (store) row base and
+  // the bytes it spans, 0 when absent -- read from lane i into scalars, so
+  // the row's buffer resource is wave-uniform
+  auto row_at = [&](const WalkRecs<NI>& r, int i, bool dst, int& n) -> char* {
+    const int64_t w = dst ? r.d : r.s;
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)(uint64_t)w, i);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)w >> 32), i);
+    const int64_t v = (int64_t)(((uint64_t)hi << 32) | lo);
+    const bool ok = __builtin_amdgcn_readlane(r.in, i) && v >= 0;
+    n = ok ? span : 0;
+    return ok ? base + v : base;
+  };
+  auto load_tile = [&](const WalkRecs<NI>& r, u32x4 (&v)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      int n;
+      const char* q = row_at(r, i, false, n);
+      v[i] = ld_row_nt(q, off, n);
+    }
+  };
+  auto store_tile = [&](const WalkRecs<NI>& r, const u32x4 (&v)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      int n;
+      char* q = row_at(r, i, true, n);
+      st_row_nt(q, off, n, v[i]);
+    }
+  };
+  WalkRecs<NI> r0, r1, r2;
+  load_recs(h, r0);
+  load_recs(h + NI, r1);
+  u32x4 va[NI], vb[NI];
+  load_tile(r0, va);  // (waits for r0 only)
+  for (int j0 = h;; j0 += 2 * NI) {
+    // tile at j0 in va (records r0), the next tile's records in r1
+    load_recs(j0 + 2 * NI, r2);
+    load_tile(r1, vb);
+    store_tile(r0, va);
+    if (j0 + NI >= nk) break;
+    load_recs(j0 + 3 * NI, r0);
+    load_tile(r2, va);
+    store_tile(r1, vb);
+    if (j0 + 2 * NI >= nk) break;
+    r1 = r0;
+    r0 = r2;
+  }
+}
+
 template <int LPR, int NI>
 hipError_t launch_move(const InplaceArgs& a, hipStream_t s) {
   const int64_t units = (int64_t)a.B * a.n_lk * a.n_slices;
@@ -387,7 +497,12 @@ hipError_t launch_compact_inplace(const InplaceArgs& a, hipStream_t s) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   switch (a.lanes_per_row * 1000 + a.tile_ni) {
-    case 64016: return launch_move<64, 16>(a, s);
+    case 64016: {
+      const int64_t units = (int64_t)a.B * a.n_lk * a.n_slices;
+      const int64_t blocks = (units + kCompactWaves - 1) / kCompactWaves;
+      hipLaunchKernelGGL((k_inplace_walk<8>), dim3((unsigned)blocks), dim3(kCompactThreads), 0, s, a);
+      return hipGetLastError();
+    }
     case 16008: return launch_move<16, 8>(a, s);
     case 16016: return launch_move<16, 16>(a, s);
     case 4004: return launch_move<4, 4>(a, s);

@@ -335,10 +335,15 @@ def test_select_split_matches_oracle_bit_exact(E, B, ld_s, K):
 # ---------------------------------------------------------------------------
 # compact: App. H
 # ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dst_layout", ["scattered", "ascending"])
 @pytest.mark.parametrize("page", [16, 8])
-def test_compact_matches_oracle_bytes(E, page):
+def test_compact_matches_oracle_bytes(E, page, dst_layout):
+    """Scattered destination pages are written in page-id order through a
+    bitmap rank; ascending ones (runs of pages, sequences in order, with
+    unused pages of short and refused sequences among them) through the
+    prefix counts.  Either order gives the same bytes."""
     import torch
-    print(f"compact page={page}", flush=True)
+    print(f"compact page={page} dst={dst_layout}", flush=True)
     g = synth.rng(400 + page)
     L, H, d, K = 4, 8, 128, 256
     Ns = np.array([37, 300, 1000, 777, 256], dtype=np.int64)
@@ -349,8 +354,13 @@ def test_compact_matches_oracle_bytes(E, page):
     pool = synth.random_bits16(g, (L, 2, n_src, page, H * d))
     pool[0, 0, src_pt[1, 0], 3, 5] = 0x7FC1          # NaN payload
     dpp = (K + page - 1) // page
-    dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g,
-                                      n_pages_total=B * dpp + 3)
+    if dst_layout == "scattered":
+        dst_pt, n_dst = synth.page_tables(np.full(B, K), page, g,
+                                          n_pages_total=B * dpp + 3)
+    else:
+        dst_pt, n_dst = synth.contiguous_page_tables(np.full(B, K), page,
+                                                     first=2)
+        n_dst += 3
     SENT = 0x5A5A
     ld_s = int(Ns.max())
     sc = np.zeros((B, ld_s), dtype=np.float32)
