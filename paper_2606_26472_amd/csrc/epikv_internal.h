@@ -307,6 +307,7 @@ constexpr int64_t kCompactGridX = 1 << 24;  // gather workgroups per grid row
 constexpr int kCompactWaves = kCompactThreads / 64;  // walks per in-place move workgroup
 constexpr int kLagWgWanted = 512;        // split a plane's rows until this many workgroups
 constexpr int kLagPtCache = 1024;        // page-table entries a KV-scorer workgroup keeps in LDS
+constexpr int kLagRowCache = kLagPtCache / 2;  // or row offsets (int64, the same LDS)
 
 // KV-vector scorer shapes (lag: a lag-normalised signal).  Wavefronts per
 // workgroup and rows each keeps in flight: 8 and 8 for the lag-normalised

@@ -22,10 +22,13 @@
 // takes a segment of 512 channels of a row (rows of 1024 channels: two
 // wavefronts per row, each writing its own partial sum), or several narrow
 // rows; with row segments the row, its page and its address are
-// wave-uniform (scalar).  Each wavefront keeps a fixed number of rows in
-// flight: the loads of the next rows are issued as soon as a pair of rows
-// has been used, unconditionally (rows past its share are empty loads), so
-// that every use waits for its own rows only.
+// wave-uniform (scalar): a wavefront walks its rows in blocks of 64 whose
+// byte offsets sit one per lane (read from an LDS table of the
+// workgroup's rows, computed once, when the chunk is short enough).  Each
+// wavefront keeps a fixed number of rows in flight: the loads of the next
+// rows are issued as soon as a pair of rows has been used, unconditionally
+// (rows past its block are empty loads), so that every use waits for its
+// own rows only.
 //   Variance, one pass: the sum and the sum of squares over the head.  For
 //   the lag-normalised signals each channel is mapped to
 //   y = (x - mn) / (mx - mn + eps) - 1/2 (the shift keeps the sums of
@@ -55,6 +58,7 @@ namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) int lds_int;
+typedef __attribute__((address_space(3))) int64_t lds_i64;
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
@@ -146,8 +150,11 @@ __device__ __forceinline__ float nan_max(float a, float b) {
 // scale, the running minimum and maximum): 512-thread workgroups of up
 // to 128 registers per lane with 8 rows in flight.  The raw signals carry
 // none: 1024-thread workgroups within 64 registers (two per CU), 4 rows in
-// flight.
-template <bool LAG, bool WIDE, int NW>
+// flight.  RT (rows of whole wavefronts, chunks of up to kLagRowCache
+// rows): the byte offsets of the workgroup's rows are computed once into
+// LDS, so the loop over the rows holds none of the page-table arithmetic
+// (which otherwise spills scalar registers).
+template <bool LAG, bool WIDE, int NW, bool RT>
 __global__ __launch_bounds__(lagkv_threads(LAG))
 __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArgs a) {
   constexpr int NCH = 2 * NW;               // channels per lane
@@ -215,21 +222,22 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   const bool any_rows = seq_ok && r_hi > r_lo;
   const int pg0 = any_rows ? page_index(start + r_lo) : 0;
   const int n_pg = any_rows ? page_index(start + r_hi - 1) - pg0 + 1 : 0;
-  const bool cached = n_pg <= kLagPtCache;
+  const bool cached = !RT && n_pg <= kLagPtCache;
   float* red = lds + (LAG ? lagkv_range_floats(a.H, a.d) : 0);
   int* lpt = reinterpret_cast<int*>(red + (WIDE ? WAVES * AH * kRedRowWords : 0));
   if (cached)
     for (int i = tid; i < n_pg; i += NT) lpt[i] = pt[pg0 + i];
-  __syncthreads();
+  // (RT: the same LDS holds the share's row offsets, filled below)
+  int64_t* lrows = reinterpret_cast<int64_t*>(lpt);
   // The plane's base and this lane's column: a row address is the base
   // plus a wave-uniform row offset (row segments), to which the lane's
   // column is added by the load itself.
   const char* pbase = a.base + (int64_t)layer * a.s_layer + (int64_t)kv * a.s_kv;
   const int loff = col * 4 * NW;
-  // Byte offset (in the plane) of chunk row r, -1 if the row is not this
-  // wavefront's or its page is out of range.
-  auto row_off = [&](int r) -> int64_t {
-    if (!seq_ok || r >= s_hi) return -1;
+  // Byte offset (in the plane) of chunk row r, -1 if the row is past `hi`
+  // or its page is out of range.
+  auto row_off = [&](int r, int hi) -> int64_t {
+    if (!seq_ok || r >= hi) return -1;
     const int pos = start + r;
     const int pidx = page_index(pos);
     // (an LDS-typed read: a generic load of either table would make the
@@ -238,25 +246,35 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
     if (pg < 0 || pg >= a.n_pages) return -1;
     return (int64_t)pg * a.s_page + (int64_t)(pos - pidx * a.page_size) * row_bytes;
   };
-  // Row segments: lane i keeps the offset of row tb + i of the wavefront's
-  // block (a table refilled every 64 rows), and a row's offset is read
-  // from it with readlane -- no memory round trip per row.
-  int tb = -(1 << 30);
+  // Row segments: a wavefront walks its rows in blocks of 64; lane i
+  // keeps the offset of row tb + i of the current block, and a row's
+  // offset is read from it with readlane -- no memory round trip per row.
+  // The table is filled at the head of each block only, so the page-table
+  // arithmetic is not live in the loop over the block's rows.
+  if (RT)
+    for (int i = tid; i < r_hi - r_lo; i += NT) lrows[i] = row_off(r_lo + i, r_hi);
+  __syncthreads();
+  int tb = 0;
   uint32_t t_lo = 0, t_hi = 0;
+  auto fill_table = [&](int it0) {
+    if (!WIDE) return;
+    tb = s_lo + it0;
+    const int r = tb + lane;
+    const int64_t o = RT ? (r < s_hi ? ((const lds_i64*)lrows)[r - r_lo] : -1) : row_off(r, s_hi);
+    t_lo = (uint32_t)o;
+    t_hi = (uint32_t)((uint64_t)o >> 32);
+  };
+  // (rows past the block are absent: they are loaded in the next block)
   auto row_addr = [&](int r, bool& ok) -> const char* {
     int64_t off;
     if (WIDE) {
-      if (r - tb >= 64 || r < tb) {
-        tb = r;
-        const int64_t o = row_off(r + lane);
-        t_lo = (uint32_t)o;
-        t_hi = (uint32_t)((uint64_t)o >> 32);
-      }
-      const uint32_t lo = __builtin_amdgcn_readlane(t_lo, r - tb);
-      const uint32_t hi = __builtin_amdgcn_readlane(t_hi, r - tb);
-      off = (int64_t)(((uint64_t)hi << 32) | lo);
+      const int i = r - tb;
+      const int ic = i < 64 ? i : 63;
+      const uint32_t lo = __builtin_amdgcn_readlane(t_lo, ic);
+      const uint32_t hi = __builtin_amdgcn_readlane(t_hi, ic);
+      off = i < 64 ? (int64_t)(((uint64_t)hi << 32) | lo) : -1;
     } else {
-      off = row_off(r);
+      off = row_off(r, s_hi);
     }
     ok = off >= 0;
     return ok ? pbase + off : pbase;
@@ -325,6 +343,7 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
     if (fresh) {
       // first pass: the chunk's own range
       for (int it = 0; it < sweeps; ++it) {
+        if (it % 64 == 0) fill_table(it);
         uint32_t w[NW];
         bool ok;
         load_row(row_of(it), w, ok);
@@ -492,22 +511,31 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   // used its registers receive the pair AH rows on.  Every load is
   // unconditional, so the loads in flight are the same on every path and
   // each use waits for its own pair only.
-  if (sweeps > 0) {
+  // (in blocks of 64 sweeps: a block's last loads reach past it and are
+  // empty; the next block starts its own)
+  for (int b0 = 0; b0 < sweeps; b0 += 64) {
+    fill_table(b0);
+    const int b1 = min(sweeps, b0 + 64);
+    // (okn: one bit per row in flight, set when the row is present)
     uint32_t raw[AH][NW];
-    bool ok[AH];
+    uint32_t okn = 0;
+    auto load_bit = [&](int r, int u) {
+      bool ok;
+      load_row(r, raw[u], ok);
+      okn = (okn & ~(1u << u)) | (ok ? 1u << u : 0u);
+    };
 #pragma unroll
-    for (int u = 0; u < AH; ++u) load_row(row_of(u), raw[u], ok[u]);
-    for (int it0 = 0;; it0 += AH) {
-      uint32_t okm = 0;
+    for (int u = 0; u < AH; ++u) load_bit(row_of(b0 + u), u);
+    for (int it0 = b0;; it0 += AH) {
+      const uint32_t okm = okn;
 #pragma unroll
       for (int u = 0; u < AH; u += 2) {
-        process_pair(it0, u, raw[u], raw[u + 1], ok[u], ok[u + 1]);
-        okm |= (ok[u] ? 1u << u : 0u) | (ok[u + 1] ? 2u << u : 0u);
-        load_row(row_of(it0 + AH + u), raw[u], ok[u]);
-        load_row(row_of(it0 + AH + u + 1), raw[u + 1], ok[u + 1]);
+        process_pair(it0, u, raw[u], raw[u + 1], (okm >> u) & 1, (okm >> (u + 1)) & 1);
+        load_bit(row_of(it0 + AH + u), u);
+        load_bit(row_of(it0 + AH + u + 1), u + 1);
       }
       if (WIDE) reduce_batch(it0, okm);
-      if (it0 + AH >= sweeps) break;
+      if (it0 + AH >= b1) break;
     }
   }
 
@@ -569,11 +597,11 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
   a.range_out[half + o] = hi;
 }
 
-template <bool LAG, bool WIDE, int NW>
+template <bool LAG, bool WIDE, int NW, bool RT = false>
 hipError_t launch_lag(const ScoreLagArgs& a, hipStream_t s) {
   const dim3 grid(a.n_planes, a.B, a.splits);
   const size_t lds = lagkv_lds_bytes(a.H, a.d, a.lag);
-  hipLaunchKernelGGL((k_score_lagkv<LAG, WIDE, NW>), grid, dim3(lagkv_threads(LAG)), lds, s, a);
+  hipLaunchKernelGGL((k_score_lagkv<LAG, WIDE, NW, RT>), grid, dim3(lagkv_threads(LAG)), lds, s, a);
   return hipGetLastError();
 }
 
@@ -589,10 +617,15 @@ size_t lagkv_lds_bytes(int H, int d, bool lag) {
 
 hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hipStream_t s) {
   const bool wide = lagkv_wide(a.H, a.d, a.lag);
-  const hipError_t e = a.lag ? (wide ? launch_lag<true, true, kLagWords>(a, s)
-                                     : launch_lag<true, false, kLagWords>(a, s))
-                             : (wide ? launch_lag<false, true, kLagWords>(a, s)
-                                     : launch_lag<false, false, kLagWords>(a, s));
+  // (a stream's first chunk is one share of all C rows, so C bounds a share)
+  const bool rt = a.C <= kLagRowCache;
+  const hipError_t e =
+      a.lag ? (!wide ? launch_lag<true, false, kLagWords>(a, s)
+               : rt  ? launch_lag<true, true, kLagWords, true>(a, s)
+                     : launch_lag<true, true, kLagWords>(a, s))
+            : (!wide ? launch_lag<false, false, kLagWords>(a, s)
+               : rt  ? launch_lag<false, true, kLagWords, true>(a, s)
+                     : launch_lag<false, true, kLagWords>(a, s));
   if (e != hipSuccess) return e;
   const int tok_blocks = (r.C + kRedTok - 1) / kRedTok;
   const int rng_blocks = r.lag && r.splits > 1 ? (r.n_chan + kScoreThreads - 1) / kScoreThreads : 0;
