@@ -161,7 +161,7 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   constexpr int WAVES = lagkv_waves(LAG);   // wavefronts per workgroup
   constexpr int NT = WAVES * 64;
   constexpr int AH = lagkv_ahead(LAG);      // rows in flight per wavefront
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -191,6 +191,26 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   // this lane's first channel in the [2][B][L][2][H][d] range layout
   const int64_t rbase = (((int64_t)b * a.L + layer) * 2 + kv) * HD + col * NCH;
   const bool fresh = LAG && a.n_tok_in[b] <= 0;
+  // The previous chunk's range of this lane's channels (carried state),
+  // loaded first as whole vectors, so that its latency overlaps the set-up
+  // of the row table instead of delaying the first rows.
+  float rin[LAG ? 2 * NCH : 1];
+  if (LAG && !fresh) {
+    const float4* qmn = reinterpret_cast<const float4*>(a.range_in + rbase);
+    const float4* qmx = reinterpret_cast<const float4*>(a.range_in + half + rbase);
+#pragma unroll
+    for (int k = 0; k < NCH / 4; ++k) {
+      const float4 u = qmn[k], v = qmx[k];
+      rin[4 * k] = u.x;
+      rin[4 * k + 1] = u.y;
+      rin[4 * k + 2] = u.z;
+      rin[4 * k + 3] = u.w;
+      rin[NCH + 4 * k] = v.x;
+      rin[NCH + 4 * k + 1] = v.y;
+      rin[NCH + 4 * k + 2] = v.z;
+      rin[NCH + 4 * k + 3] = v.w;
+    }
+  }
   // this segment's row of partial sums [B][plane][segment][C]
   float* part = a.partial + (((int64_t)b * a.n_planes + p) * segs + seg) * a.C;
 
@@ -309,26 +329,34 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   auto deposit = [&]() {
     float* sl = lds + (int64_t)vid * 2 * HD + col * NCH;
 #pragma unroll
-    for (int e = 0; e < NCH; ++e) {
-      sl[e] = cmn[e];
-      sl[HD + e] = cmx[e];
+    for (int e = 0; e < NCH; e += 4) {
+      *reinterpret_cast<float4*>(sl + e) = make_float4(cmn[e], cmn[e + 1], cmn[e + 2], cmn[e + 3]);
+      *reinterpret_cast<float4*>(sl + HD + e) =
+          make_float4(cmx[e], cmx[e + 1], cmx[e + 2], cmx[e + 3]);
     }
   };
   const int64_t plane_off = (((int64_t)b * a.L + layer) * 2 + kv) * HD;
   auto combine = [&](bool keep) {
     __syncthreads();
     float* dst = a.splits == 1 ? a.range_out : a.prange + (int64_t)sp * 2 * half;
-    for (int i = tid; i < 2 * HD; i += NT) {
-      float v = lds[i];
+    // four channels per thread and step (each half holds whole groups of 4)
+    for (int i = 4 * tid; i < 2 * HD; i += 4 * NT) {
+      const bool lo = i < HD;
+      float4 v = *reinterpret_cast<const float4*>(lds + i);
       for (int k = 1; k < n_part; ++k) {
-        const float o = lds[(int64_t)k * 2 * HD + i];
-        v = i < HD ? nan_min(v, o) : nan_max(v, o);
+        const float4 o = *reinterpret_cast<const float4*>(lds + (int64_t)k * 2 * HD + i);
+        v.x = lo ? nan_min(v.x, o.x) : nan_max(v.x, o.x);
+        v.y = lo ? nan_min(v.y, o.y) : nan_max(v.y, o.y);
+        v.z = lo ? nan_min(v.z, o.z) : nan_max(v.z, o.z);
+        v.w = lo ? nan_min(v.w, o.w) : nan_max(v.w, o.w);
       }
-      dst[(i < HD ? 0 : half - HD) + plane_off + i] = v;
-      if (keep) lds[i] = v;
+      const int64_t at = (lo ? 0 : half - HD) + plane_off + i;
+      *reinterpret_cast<float4*>(dst + at) = v;
+      if (keep) *reinterpret_cast<float4*>(lds + i) = v;
       if (a.splits == 1 && !a.two) {
         // a one-tensor signal carries no range for the other tensor
-        a.range_out[(i < HD ? 0 : half - HD) + plane_off + (int64_t)(1 - 2 * kv) * HD + i] = 0.f;
+        *reinterpret_cast<float4*>(a.range_out + at + (int64_t)(1 - 2 * kv) * HD) =
+            make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
     __syncthreads();
@@ -361,8 +389,8 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
     }
 #pragma unroll
     for (int e = 0; e < NCH; ++e) {
-      const float mn = fresh ? lds[col * NCH + e] : a.range_in[rbase + e];
-      const float mx = fresh ? lds[HD + col * NCH + e] : a.range_in[half + rbase + e];
+      const float mn = fresh ? lds[col * NCH + e] : rin[e];
+      const float mx = fresh ? lds[HD + col * NCH + e] : rin[NCH + e];
       mnv[e] = mn;
       sc[e] = 1.0f / (mx - mn + a.eps);
     }
