@@ -392,7 +392,7 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
       const float mn = fresh ? lds[col * NCH + e] : rin[e];
       const float mx = fresh ? lds[HD + col * NCH + e] : rin[NCH + e];
       mnv[e] = mn;
-      sc[e] = 1.0f / (mx - mn + a.eps);
+      sc[e] = __builtin_amdgcn_rcpf(mx - mn + a.eps);  // (one reciprocal instruction)
     }
   }
 
@@ -475,10 +475,17 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
       auto sums = [&](float xa, float xb, int e) {
         const float ya = fmaf(xa - mnv[e], sc[e], -0.5f);
         const float yb = fmaf(xb - mnv[e], sc[e], -0.5f);
-        sa += ya;
-        qa = fmaf(ya, ya, qa);
-        sb += yb;
-        qb = fmaf(yb, yb, qb);
+        if (e == 0) {  // (the sums start at the first channel, not at 0 + y)
+          sa = ya;
+          qa = ya * ya;
+          sb = yb;
+          qb = yb * yb;
+        } else {
+          sa += ya;
+          qa = fmaf(ya, ya, qa);
+          sb += yb;
+          qb = fmaf(yb, yb, qb);
+        }
       };
       if (track_range && oka && okb) {
         // both rows present: three-input minimum / maximum
