@@ -100,8 +100,10 @@ int lag_planes(const epikv_cfg* c) {
 int lag_splits(const epikv_cfg* c, int chunk) {
   const bool lag = uses_range(c->signal);
   const int64_t base = (int64_t)lag_planes(c) * c->batch;
-  const int64_t s = (kLagWgWanted + base - 1) / base;
-  const int64_t cap = std::max<int64_t>(1, chunk / (lagkv_waves(lag) * lagkv_ahead(lag)));
+  const bool big = lagkv_big(c->n_kv_heads, c->head_dim, lag, base);
+  const int64_t wanted = big ? kLagWgWanted / 2 : kLagWgWanted;
+  const int64_t s = (wanted + base - 1) / base;
+  const int64_t cap = std::max<int64_t>(1, chunk / (lagkv_waves(lag, big) * lagkv_ahead(lag)));
   return (int)std::max<int64_t>(1, std::min(s, cap));
 }
 

@@ -312,16 +312,18 @@ constexpr int kLagRowCache = kLagPtCache / 2;  // or row offsets (int64, the sam
 // KV-vector scorer shapes (lag: a lag-normalised signal).  Wavefronts per
 // workgroup and rows each keeps in flight: 8 and 8 for the lag-normalised
 // signals, whose four registers of per-channel state allow four
-// wavefronts per SIMD; 16 and 4 for the raw signals, which fit eight.
+// wavefronts per SIMD (two workgroups per CU); 16 and 4 for the raw
+// signals, which fit eight.  When the planes and sequences alone give at
+// most kLagWgWanted / 2 workgroups (one lag-normalised tensor), its
+// workgroups are "big": 16 wavefronts (one workgroup per CU) with 8 rows
+// in flight each, which cover a plane's rows in half as many shares and
+// so spare the partial ranges of the split rows.
 // A lane takes 4 words (8 channels, 16 bytes) of a row, so a row spans
 // H*d / 8 lanes; from 64 lanes on it is split into segments of 64 lanes,
 // one wavefront each.
 // LDS: the range slots (lag-normalised only; one [2][H*d] slot per row
 // slot, or per row of a wavefront for narrow rows), then the transposed
 // reduction's rows (row segments), then kLagPtCache page-table entries.
-__host__ __device__ constexpr int lagkv_waves(bool lag) { return lag ? 8 : 16; }
-__host__ __device__ constexpr int lagkv_threads(bool lag) { return 64 * lagkv_waves(lag); }
-__host__ __device__ constexpr int lagkv_ahead(bool lag) { return lag ? 8 : 4; }
 constexpr int kLagWords = 4;
 __host__ __device__ inline int lagkv_row_lanes(int H, int d, bool) { return H * d / (2 * kLagWords); }
 __host__ __device__ inline bool lagkv_wide(int H, int d, bool lag) {
@@ -331,16 +333,25 @@ __host__ __device__ inline int lagkv_segments(int H, int d, bool lag) {
   const int lanes = lagkv_row_lanes(H, d, lag);
   return lanes >= 64 ? lanes / 64 : 1;
 }
-__host__ __device__ inline int lagkv_range_floats(int H, int d) {
+// base: used planes x sequences
+__host__ __device__ inline bool lagkv_big(int H, int d, bool lag, int64_t base) {
+  return lag && lagkv_wide(H, d, lag) && base <= kLagWgWanted / 2;
+}
+__host__ __device__ constexpr int lagkv_waves(bool lag, bool big) { return lag && !big ? 8 : 16; }
+__host__ __device__ constexpr int lagkv_threads(bool lag, bool big) {
+  return 64 * lagkv_waves(lag, big);
+}
+__host__ __device__ constexpr int lagkv_ahead(bool lag) { return lag ? 8 : 4; }
+__host__ __device__ inline int lagkv_range_floats(int H, int d, bool big) {
   const int lanes = lagkv_row_lanes(H, d, true);
-  const int n_part = lanes >= 64 ? lagkv_waves(true) / lagkv_segments(H, d, true)
-                                 : lagkv_waves(true) * (64 / lanes);
+  const int n_part = lanes >= 64 ? lagkv_waves(true, big) / lagkv_segments(H, d, true)
+                                 : lagkv_waves(true, big) * (64 / lanes);
   return n_part * 2 * H * d;
 }
 // The transposed reduction's row of 64 (sum, sum of squares) pairs, with
 // 4 words of padding after every 8 lanes.
 constexpr int kRedRowWords = 64 * 2 + 8 * 4;
-size_t lagkv_lds_bytes(int H, int d, bool lag);
+size_t lagkv_lds_bytes(int H, int d, bool lag, bool big);
 constexpr int kInplaceThreads = 1024;    // per-sequence check + score move
 constexpr int kInplaceUnitsWanted = 2048;  // narrow the column slices below this
 

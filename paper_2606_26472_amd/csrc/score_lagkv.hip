@@ -154,11 +154,11 @@ __device__ __forceinline__ float nan_max(float a, float b) {
 // rows): the byte offsets of the workgroup's rows are computed once into
 // LDS, so the loop over the rows holds none of the page-table arithmetic
 // (which otherwise spills scalar registers).
-template <bool LAG, bool WIDE, int NW, bool RT>
-__global__ __launch_bounds__(lagkv_threads(LAG))
+template <bool LAG, bool WIDE, int NW, bool RT, bool BIG>
+__global__ __launch_bounds__(lagkv_threads(LAG, BIG))
 __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArgs a) {
   constexpr int NCH = 2 * NW;               // channels per lane
-  constexpr int WAVES = lagkv_waves(LAG);   // wavefronts per workgroup
+  constexpr int WAVES = lagkv_waves(LAG, BIG);  // wavefronts per workgroup
   constexpr int NT = WAVES * 64;
   constexpr int AH = lagkv_ahead(LAG);      // rows in flight per wavefront
   extern __shared__ __align__(16) float lds[];
@@ -243,7 +243,7 @@ __attribute__((amdgpu_waves_per_eu(LAG ? 4 : 8))) void k_score_lagkv(ScoreLagArg
   const int pg0 = any_rows ? page_index(start + r_lo) : 0;
   const int n_pg = any_rows ? page_index(start + r_hi - 1) - pg0 + 1 : 0;
   const bool cached = !RT && n_pg <= kLagPtCache;
-  float* red = lds + (LAG ? lagkv_range_floats(a.H, a.d) : 0);
+  float* red = lds + (LAG ? lagkv_range_floats(a.H, a.d, BIG) : 0);
   int* lpt = reinterpret_cast<int*>(red + (WIDE ? WAVES * AH * kRedRowWords : 0));
   if (cached)
     for (int i = tid; i < n_pg; i += NT) lpt[i] = pt[pg0 + i];
@@ -632,20 +632,21 @@ __global__ __launch_bounds__(kScoreThreads) void k_lag_reduce(LagReduceArgs a) {
   a.range_out[half + o] = hi;
 }
 
-template <bool LAG, bool WIDE, int NW, bool RT = false>
+template <bool LAG, bool WIDE, int NW, bool RT = false, bool BIG = false>
 hipError_t launch_lag(const ScoreLagArgs& a, hipStream_t s) {
   const dim3 grid(a.n_planes, a.B, a.splits);
-  const size_t lds = lagkv_lds_bytes(a.H, a.d, a.lag);
-  hipLaunchKernelGGL((k_score_lagkv<LAG, WIDE, NW, RT>), grid, dim3(lagkv_threads(LAG)), lds, s, a);
+  const size_t lds = lagkv_lds_bytes(a.H, a.d, a.lag, BIG);
+  hipLaunchKernelGGL((k_score_lagkv<LAG, WIDE, NW, RT, BIG>), grid, dim3(lagkv_threads(LAG, BIG)),
+                     lds, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-size_t lagkv_lds_bytes(int H, int d, bool lag) {
-  return (lag ? lagkv_range_floats(H, d) * sizeof(float) : 0) +
+size_t lagkv_lds_bytes(int H, int d, bool lag, bool big) {
+  return (lag ? lagkv_range_floats(H, d, big) * sizeof(float) : 0) +
          (lagkv_wide(H, d, lag)
-              ? (size_t)lagkv_waves(lag) * lagkv_ahead(lag) * kRedRowWords * sizeof(float)
+              ? (size_t)lagkv_waves(lag, big) * lagkv_ahead(lag) * kRedRowWords * sizeof(float)
               : 0) +
          kLagPtCache * sizeof(int);
 }
@@ -654,10 +655,13 @@ hipError_t launch_score_lagkv(const ScoreLagArgs& a, const LagReduceArgs& r, hip
   const bool wide = lagkv_wide(a.H, a.d, a.lag);
   // (a stream's first chunk is one share of all C rows, so C bounds a share)
   const bool rt = a.C <= kLagRowCache;
+  const bool big = lagkv_big(a.H, a.d, a.lag, (int64_t)a.n_planes * a.B);
   const hipError_t e =
       a.lag ? (!wide ? launch_lag<true, false, kLagWords>(a, s)
-               : rt  ? launch_lag<true, true, kLagWords, true>(a, s)
-                     : launch_lag<true, true, kLagWords>(a, s))
+               : rt  ? (big ? launch_lag<true, true, kLagWords, true, true>(a, s)
+                            : launch_lag<true, true, kLagWords, true>(a, s))
+                     : (big ? launch_lag<true, true, kLagWords, false, true>(a, s)
+                            : launch_lag<true, true, kLagWords>(a, s)))
             : (!wide ? launch_lag<false, false, kLagWords>(a, s)
                : rt  ? launch_lag<false, true, kLagWords, true>(a, s)
                      : launch_lag<false, true, kLagWords>(a, s));

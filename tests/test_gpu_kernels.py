@@ -446,14 +446,22 @@ def test_kv_signal_nan_propagates_as_in_the_oracle(E, signal):
     _run_kv(E, signal, 64, nan=True)
 
 
-def _run_kv(E, signal, C, nan=False, H=8, d=128):
+@pytest.mark.parametrize("signal,L", [("lagkv", 65), ("lagkv_key", 129)])
+def test_kv_signals_many_planes(E, signal, L):
+    """More than 256 (used plane, sequence) pairs: the lag-normalised
+    signals then take 8-wavefront workgroups, two per CU (fewer pairs take
+    16-wavefront ones, one per CU)."""
+    _run_kv(E, signal, 37, L=L)
+
+
+def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4):
     import torch
-    print(f"kv signal {signal} C={C} nan={nan} H={H} d={d}", flush=True)
+    print(f"kv signal {signal} C={C} nan={nan} H={H} d={d} L={L}", flush=True)
     use_k, use_v, lag = KV_SIGNALS[signal]
     sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
               "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
     g = synth.rng(500)
-    L, page, B, w = 4, 16, 2, 64
+    page, B, w = 16, 2, 64
     n_chunks = 3
     T = C * n_chunks
     Ns = np.array([T, T + 16])       # seq 1 has 16 older tokens first
