@@ -49,6 +49,9 @@ __global__ __launch_bounds__(kZscoreThreads) void k_score_tokens(ScoreTokArgs a)
     const bool active = l < a.n_band;
     if (active) {
       const int64_t row = (int64_t)b * a.n_band + l;
+      // (the carried EMA value is loaded first: it is only used after the
+      // rows, so its latency overlaps theirs)
+      const float ema_c = a.ema_in[row];
       for (int k = lane; k < wm1; k += 64) x[k] = a.ring_in[row * wm1 + k];
       // Eq. 1 over the chunk's rows, the previous row in registers
       const uint16_t* rows = a.hidden[l] + (int64_t)b * a.ld_seq;
@@ -81,15 +84,21 @@ __global__ __launch_bounds__(kZscoreThreads) void k_score_tokens(ScoreTokArgs a)
           if (lane == 0 && c + u < a.C)
             x[wm1 + c + u] = (fresh && c + u == 0) ? 0.f : sqrtf(g2);
         }
+        // (prev: the latest row of the chunk, so after the loop its last)
 #pragma unroll
-        for (int i = 0; i < VPW; ++i) prev[i] = cur[U - 1][i];
+        for (int u = 0; u < U; ++u)
+          if (c + u < a.C)
+#pragma unroll
+            for (int i = 0; i < VPW; ++i) prev[i] = cur[u][i];
       }
-      // the chunk's last row is the next call's predecessor
-      const uint16_t* last = rows + (int64_t)(a.C - 1) * a.ld_tok;
+      // the chunk's last row is the next call's predecessor (from registers)
       uint16_t* hout = a.h_prev_out + row * a.D;
-      for (int v = lane; v < nvec; v += 64)
-        *reinterpret_cast<u32x4*>(hout + v * 8) = *reinterpret_cast<const u32x4*>(last + v * 8);
-      if (lane == 0) carry[l] = a.ema_in[row];
+#pragma unroll
+      for (int i = 0; i < VPW; ++i) {
+        const int v = lane + i * 64;
+        if (v < nvec) *reinterpret_cast<u32x4*>(hout + v * 8) = prev[i];
+      }
+      if (lane == 0) carry[l] = ema_c;
     }
     __syncthreads();
     if (active) {
