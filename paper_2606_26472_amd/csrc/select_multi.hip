@@ -203,12 +203,21 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_multi(SelectMultiArgs
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  constexpr int kSpan = KPT * kSelectThreads;
+  const int g0 = g * kSpan;  // first position of this workgroup's slice
+  // The slice's scores are loaded first: their addresses do not depend on
+  // the sequence's counts, so the two loads are in flight together.
+  const float* s = a.scores + (int64_t)b * a.ld_s;
+  float raw[KPT];
+#pragma unroll
+  for (int k = 0; k < KPT; ++k) {
+    const int i = g0 + k * kSelectThreads + tid;
+    raw[k] = i < a.ld_s ? s[i] : 0.f;
+  }
   const int N = a.n_cached[b];
   const int P = a.n_prefix[b];
   const int K = a.K;
   const int R = a.R;
-  constexpr int kSpan = KPT * kSelectThreads;
-  const int g0 = g * kSpan;  // first position of this workgroup's slice
   int32_t* out = a.keep_idx + (int64_t)b * K;
 
   // Decisions that end a sequence early are the same in all its workgroups,
@@ -237,14 +246,13 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_multi(SelectMultiArgs
     return;
   }
 
-  // The keys are loaded first, so that the look at the marker overlaps them.
-  const float* s = a.scores + (int64_t)b * a.ld_s;
+  // (the look at the marker overlaps the scores' loads)
   const int lo = P, hi = N - R;  // eligible positions [lo, hi)
   uint32_t keys[KPT];
 #pragma unroll
   for (int k = 0; k < KPT; ++k) {
     const int i = g0 + k * kSelectThreads + tid;
-    keys[k] = (i >= lo && i < hi) ? rank_key(s[i]) : 0u;
+    keys[k] = (i >= lo && i < hi) ? rank_key(raw[k]) : 0u;
   }
 
   uint32_t* seq = m.scratch + (size_t)b * kSelSeqWords;
