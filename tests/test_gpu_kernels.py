@@ -419,11 +419,13 @@ KV_SIGNALS = {  # name: (use keys, use values, lag-normalised)
     "kv_val": (False, True, False), "lagkv_key": (True, False, True)}
 
 
-@pytest.mark.parametrize("C", [64, 37, 200, 1])
+@pytest.mark.parametrize("C", [64, 37, 200, 1, 300, 1000])
 @pytest.mark.parametrize("signal", list(KV_SIGNALS))
 def test_kv_signals_match_oracle(E, signal, C):
     """Chunk lengths that split a plane's rows between several workgroups
-    evenly (64), unevenly (37, 200) and not at all (1)."""
+    evenly (64), unevenly (37, 200) and not at all (1); 300 and 1000 rows
+    split a stream's first chunk too (its own range then comes from
+    several workgroups), with the row offsets in LDS (300) or not (1000)."""
     _run_kv(E, signal, C)
 
 
@@ -489,7 +491,10 @@ def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4):
           for _ in range(2)]
     E.epikv_state_init(cfg, st[0])
     ws_n = E.workspace_bytes(cfg, C)
-    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    # the workspace's contents are the caller's (here: bytes 0x7F, floats of
+    # 3.4e38, as a stale partial range would leave them): nothing the call
+    # reads may come from them
+    ws = torch.full((ws_n,), 0x7F, dtype=torch.uint8, device="cuda")
     pool_t = dev(pool)
     P = E.pool_of(pool_t.view(L, 2, n_pages, page, H, d))
     ld_s = int(Ns.max())
