@@ -424,8 +424,9 @@ KV_SIGNALS = {  # name: (use keys, use values, lag-normalised)
 def test_kv_signals_match_oracle(E, signal, C):
     """Chunk lengths that split a plane's rows between several workgroups
     evenly (64), unevenly (37, 200) and not at all (1); 300 and 1000 rows
-    split a stream's first chunk too (its own range then comes from
-    several workgroups), with the row offsets in LDS (300) or not (1000)."""
+    with the workgroup's row offsets in an LDS table (300) or computed per
+    block of 64 rows from the page table (1000, past that table's size),
+    and a first chunk whose rows the first share walks alone."""
     _run_kv(E, signal, C)
 
 
