@@ -223,6 +223,52 @@ def test_smooth_stream_skips_tokens_without_sample():
     assert out.tolist() == [0.0, 1.0, 2.0]
 
 
+def test_smooth_stream_raw_is_the_signal_itself():
+    # App. E's unsmoothed baseline: each token's own sample, whatever came
+    # before it; tokens without a sample get 0
+    new = np.array([3.5, -2.0, 7.0, 0.25])
+    has = np.array([True, False, True, True])
+    for prior in (np.zeros(0), synth.rng(30).standard_normal(100)):
+        out = O.smooth_stream(prior, new, has, O.SMOOTH_RAW, W, EPS)
+        assert out.tolist() == [3.5, 0.0, 7.0, 0.25]
+
+
+def test_smooth_stream_ema_hand_values_and_carry():
+    # App. E: y(t) = 0.9 y(t-1) + 0.1 x(t), the stream's first sample
+    # starting the average
+    out = O.smooth_stream(np.zeros(0), np.array([4.0, 0.0, 10.0]),
+                          np.ones(3, bool), O.SMOOTH_EMA, W, EPS)
+    assert np.allclose(out, [4.0, 3.6, 4.24], rtol=1e-15, atol=0)
+    # the same stream cut after two samples: the average carries over,
+    # from the earlier samples or given explicitly
+    cut = O.smooth_stream(np.array([4.0, 0.0]), np.array([10.0]),
+                          np.ones(1, bool), O.SMOOTH_EMA, W, EPS)
+    assert np.allclose(cut, [4.24], rtol=1e-15, atol=0)
+    given = O.smooth_stream(np.zeros(0), np.array([2.0]), np.ones(1, bool),
+                            O.SMOOTH_EMA, W, EPS, ema_before=1.0)
+    assert np.allclose(given, [1.1], rtol=1e-15, atol=0)
+    # a token without a sample neither moves the average nor gets a value
+    skip = O.smooth_stream(np.zeros(0), np.array([10.0, 99.0, 0.0]),
+                           np.array([True, False, True]), O.SMOOTH_EMA, W,
+                           EPS, ema_before=0.0)
+    assert np.allclose(skip, [1.0, 0.0, 0.9], rtol=1e-15, atol=0)
+
+
+def test_smooth_stream_mean_in_chunks_equals_one_pass():
+    # Eq. 2's trailing mean only looks back w-1 samples, so carrying the
+    # last w-1 samples between chunks reproduces the one-pass values
+    x = synth.rng(31).standard_normal(300)
+    full = O.rolling_mean(x, W)
+    out = []
+    prior = np.zeros(0)
+    for lo in range(0, 300, 50):
+        new = x[lo:lo + 50]
+        out.append(O.smooth_stream(prior, new, np.ones(new.size, bool),
+                                   O.SMOOTH_MEAN, W, EPS))
+        prior = np.concatenate([prior, new])[-(W - 1):]
+    assert np.array_equal(np.concatenate(out), full)
+
+
 # ---------------------------------------------------------------------------
 # Band combination (Fig. 1, Eq. 3 text)
 # ---------------------------------------------------------------------------
