@@ -78,6 +78,15 @@ MUTATIONS = {
         "    return int(moved[0]) + 1 if moved.size else int(keep.size)"),
     "inplace_clears_the_tail": ("    out = rows.copy()\n    out[:keep.size] = rows[keep]",
                                 "    out = np.zeros_like(rows)\n    out[:keep.size] = rows[keep]"),
+    # App. H page remapping: which pages qualify, where released pages go
+    "remap_unaligned_source_page": (
+        "        if r == 0 and p > m and np.array_equal(run, np.arange(p * ps, (p + 1) * ps)):",
+        "        if p > m and np.array_equal(run, np.arange(run[0], run[0] + ps)):"),
+    "remap_page_already_in_place": (
+        "        if r == 0 and p > m and np.array_equal(run, np.arange(p * ps, (p + 1) * ps)):",
+        "        if r == 0 and p >= m and np.array_equal(run, np.arange(p * ps, (p + 1) * ps)):"),
+    "remap_released_in_reverse": ("    for m, p in zip(released, losing):",
+                                  "    for m, p in zip(released[::-1], losing):"),
     # App. E: EMA weighting and start
     "ema_weights_swapped": (
         "        y = x[i] if y is None else alpha * y + (1.0 - alpha) * x[i]",
