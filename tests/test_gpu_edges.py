@@ -53,7 +53,7 @@ CASES = {
 
 def _run_case(E, name, K=64, recent=-1, window=64, C=32, page=16, H=8, d=128,
               L=2, D=256, na=2, nb=2, prefix=None, lengths=(300,),
-              nan=False):
+              nan=False, mode="z"):
     import torch
     g = synth.rng(zlib.crc32(name.encode()))
     lengths = np.asarray(lengths, np.int64)
@@ -64,7 +64,9 @@ def _run_case(E, name, K=64, recent=-1, window=64, C=32, page=16, H=8, d=128,
     HD = H * d
     cfg = E.default_cfg(batch=B, hidden=D, n_layers=L, n_kv_heads=H,
                         head_dim=d, page_size=page, n_band_a=na, n_band_b=nb,
-                        window=window, budget=K, recent=recent)
+                        window=window, budget=K, recent=recent,
+                        smoothing={"z": E.SMOOTH_Z, "mean": E.SMOOTH_MEAN,
+                                   "raw": E.SMOOTH_RAW}[mode])
     assert E.check_cfg(cfg) == 0
     R = recent if recent >= 0 else O.default_recent(K)
     Cc = min(C, int(lengths.min()))                 # chunk fits every N
@@ -124,7 +126,8 @@ def _run_case(E, name, K=64, recent=-1, window=64, C=32, page=16, H=8, d=128,
                  for l in range(nband)]
         s_new, *_ = O.hs_chunk_scores(
             O.bf16_to_float64(hid[:, b]), O.bf16_to_float64(before[b]),
-            prior, na, nb, O.SMOOTH_Z, window)
+            prior, na, nb, {"z": O.SMOOTH_Z, "mean": O.SMOOTH_MEAN,
+                            "raw": O.SMOOTH_RAW}[mode], window)
         # band differences of z-scores (can sit at 0); NaN where the
         # oracle has NaN
         assert rel_err(gs[b, N - Cc:N], s_new, NEAR_ZERO) <= TOL, (name, b)
@@ -153,3 +156,38 @@ def _run_case(E, name, K=64, recent=-1, window=64, C=32, page=16, H=8, d=128,
 def test_edge_case(E, name):
     print(f"edge case {name}", flush=True)
     _run_case(E, name, **CASES[name])
+
+
+def _random_cases(n, seed=20261202):
+    """Seeded mixes of the step's dimensions (budget, recency window,
+    window length, chunk, page size, head shape, layers, hidden width, band
+    sizes, prefill, smoothing, ragged lengths), each checked like the cases
+    above: scores, kept sets and every rebuilt byte."""
+    g = np.random.default_rng(seed)
+    out = {}
+    for i in range(n):
+        B = int(g.integers(1, 6))
+        H, d = [(1, 64), (8, 128), (3, 128), (2, 256), (4, 64)][g.integers(5)]
+        K = int(g.choice([1, 16, 64, 100, 256]))
+        lengths = g.integers(1, 700, size=B)
+        recent = int(g.choice([-1, -1, 0, int(g.integers(0, K + 1))]))
+        R = recent if recent >= 0 else O.default_recent(K)
+        prefix = [int(g.integers(0, max(1, min(n_, K - R)))) for n_ in lengths]
+        out[f"random{i}"] = dict(
+            K=K, recent=recent, window=int(g.choice([1, 5, 64, 100])),
+            C=int(g.choice([1, 7, 32, 64, 129])),
+            page=int(g.choice([1, 3, 16, 64])), H=H, d=d,
+            L=int(g.integers(1, 4)), D=int(g.choice([8, 256, 1000, 4096])),
+            na=int(g.integers(1, 5)), nb=int(g.integers(0, 5)),
+            prefix=prefix, lengths=[int(x) for x in lengths],
+            mode=str(g.choice(["z", "mean", "raw"])))
+    return out
+
+
+RANDOM_CASES = _random_cases(16)
+
+
+@pytest.mark.parametrize("name", list(RANDOM_CASES))
+def test_random_step_case(E, name):
+    print(f"random step case {name}: {RANDOM_CASES[name]}", flush=True)
+    _run_case(E, name, **RANDOM_CASES[name])
