@@ -107,6 +107,15 @@ def lib() -> ctypes.CDLL:
         raise ImportError(
             f"{LIB_PATH} is missing: build the HIP library first "
             "(python -m paper_2606_26472_amd.build)")
+    # The device buffers handed to the library are torch's, and the torch
+    # wheel carries its own HIP runtime under the same soname as the
+    # system's (libamdhip64.so.7).  Importing torch first makes the library
+    # bind to that runtime; opened first, it would bring in the system copy
+    # as a second runtime, whose launches fail on torch's allocations.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
     i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
