@@ -457,17 +457,18 @@ def test_kv_signals_many_planes(E, signal, L):
     _run_kv(E, signal, 37, L=L)
 
 
-def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4):
+def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4, B=2, page=16):
     import torch
-    print(f"kv signal {signal} C={C} nan={nan} H={H} d={d} L={L}", flush=True)
+    print(f"kv signal {signal} C={C} nan={nan} H={H} d={d} L={L} B={B} "
+          f"page={page}", flush=True)
     use_k, use_v, lag = KV_SIGNALS[signal]
     sig_id = {"lagkv": E.SIGNAL_LAGKV, "kv_key": E.SIGNAL_KV_KEY,
               "kv_val": E.SIGNAL_KV_VAL, "lagkv_key": E.SIGNAL_LAGKV_KEY}[signal]
     g = synth.rng(500)
-    page, B, w = 16, 2, 64
+    w = 64
     n_chunks = 3
     T = C * n_chunks
-    Ns = np.array([T, T + 16])       # seq 1 has 16 older tokens first
+    Ns = T + 16 * np.arange(B)       # sequence b has 16 b older tokens first
     pt, n_pages = synth.page_tables(Ns, page, g)
     pool = np.zeros((L, 2, n_pages, page, H * d), dtype=np.uint16)
     tok = []   # logical rows per sequence [N][L][2][H*d]
@@ -487,7 +488,8 @@ def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4):
         pos = np.arange(Ns[b])
         pool[:, :, pt[b, pos // page], pos % page] = rows.transpose(1, 2, 0, 3)
     cfg = E.default_cfg(batch=B, n_layers=L, n_kv_heads=H, head_dim=d,
-                        signal=sig_id, smoothing=E.SMOOTH_MEAN, budget=4096)
+                        page_size=page, signal=sig_id,
+                        smoothing=E.SMOOTH_MEAN, budget=4096)
     st = [torch.zeros(E.state_bytes(cfg), dtype=torch.uint8, device="cuda")
           for _ in range(2)]
     E.epikv_state_init(cfg, st[0])
@@ -543,3 +545,31 @@ def _run_kv(E, signal, C, nan=False, H=8, d=128, L=4):
             if nan and b == 0 and j == 0:
                 assert np.isnan(got_s[b, lo:lo + C]).any()
         st = [st[1], st[0]]
+
+
+def _random_kv_cases(n, seed=20261203):
+    """Seeded mixes of signal, chunk length, head shape (H*d / 8 dividing
+    256), layers, sequences and page size for the KV-vector scorers."""
+    g = np.random.default_rng(seed)
+    shapes = [(1, 64), (2, 64), (1, 128), (4, 64), (2, 128), (8, 64),
+              (4, 128), (2, 256), (8, 128), (16, 64), (4, 256), (8, 256),
+              (16, 128)]
+    out = []
+    for _ in range(n):
+        H, d = shapes[g.integers(len(shapes))]
+        out.append(dict(signal=str(g.choice(list(KV_SIGNALS))),
+                        C=int(g.choice([1, 2, 9, 63, 64, 65, 130, 257, 520])),
+                        H=H, d=d, L=int(g.integers(1, 7)),
+                        B=int(g.integers(1, 6)),
+                        page=int(g.choice([1, 3, 16, 64]))))
+    return out
+
+
+RANDOM_KV = _random_kv_cases(16)
+
+
+@pytest.mark.parametrize("i", range(len(RANDOM_KV)))
+def test_kv_signals_random_shapes(E, i):
+    """Every KV-vector signal over three chained chunks (the first from a
+    fresh stream) against the oracle, on random mixes of shapes."""
+    _run_kv(E, **RANDOM_KV[i])
