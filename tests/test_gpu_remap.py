@@ -224,3 +224,34 @@ def test_remap_twice_in_a_row(E):
         assert np.array_equal(host(pt_d), exp_pt), rep
         assert host(pool_d).tobytes() == exp.tobytes(), rep
         cur = np.minimum(n_keep + 20, lengths)
+
+
+def _random_cases(n, seed):
+    """Seeded mixes of lengths, budget, layers, head shape, page size and
+    prefill (kept sets from the selection rule, or of each remapping kind)."""
+    g = np.random.default_rng(seed)
+    shapes = [(1, 64), (8, 128), (3, 128), (8, 256), (2, 64)]
+    out = {}
+    for i in range(n):
+        B = int(g.integers(1, 7))
+        H, d = shapes[g.integers(len(shapes))]
+        page = int(g.choice([1, 2, 3, 16, 64]))
+        K = int(g.choice([8, 40, 64, 130, 512]))
+        lengths = [int(x) for x in g.integers(1, 900, size=B)]
+        case = dict(lengths=lengths, K=K, L=int(g.integers(1, 5)), H=H, d=d,
+                    page=page, kind=str(g.choice(["blocks", "mixed", "select"])))
+        if g.random() < 0.5:
+            R = min(128, K // 4)
+            case["prefix"] = [int(g.integers(0, max(1, min(n_, K - R))))
+                              for n_ in lengths]
+        out[f"random{i}"] = case
+    return out
+
+
+RANDOM_CASES = _random_cases(12, 20261205)
+
+
+@pytest.mark.parametrize("name", list(RANDOM_CASES))
+def test_random_case(E, name):
+    print(f"random case {name}: {RANDOM_CASES[name]}", flush=True)
+    _run(E, name, **RANDOM_CASES[name])
