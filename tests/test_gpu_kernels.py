@@ -573,3 +573,22 @@ def test_kv_signals_random_shapes(E, i):
     """Every KV-vector signal over three chained chunks (the first from a
     fresh stream) against the oracle, on random mixes of shapes."""
     _run_kv(E, **RANDOM_KV[i])
+
+
+def _random_select_shapes(n, seed=20261206):
+    """Seeded (B, row length, K) for the split selection: rows longer than
+    K, B * row length within 2 M positions (the oracle sorts in Python)."""
+    g = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        K = int(g.choice([1, 7, 64, 300, 1024, 4096, 8192, 16384]))
+        B = int(g.choice([1, 2, 3, 5, 8, 17, 32, 64, 128]))
+        ld_s = int(g.integers(K + 1, K + 1 + 100000))
+        if B * ld_s <= 2_000_000:
+            out.append((B, ld_s, K))
+    return out
+
+
+@pytest.mark.parametrize("B,ld_s,K", _random_select_shapes(10))
+def test_select_split_random_shapes(E, B, ld_s, K):
+    test_select_split_matches_oracle_bit_exact(E, B, ld_s, K)
