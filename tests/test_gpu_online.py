@@ -281,3 +281,51 @@ def test_online_step_equals_the_scoring_step(E):
     for x, y, what in zip(a, b, ["scores", "cache", "compacted scores",
                                  "keep_idx", "n_keep", "status", "state"]):
         assert x.tobytes() == y.tobytes(), what
+
+
+def _random_online_cases(n, seed=20261207):
+    g = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        T = int(g.integers(1, 200))
+        cuts = []
+        left = T
+        while left:
+            c = int(min(left, g.choice([1, 1, 2, 3, 17, 63, 64])))
+            cuts.append(c)
+            left -= c
+        out.append(dict(B=int(g.integers(1, 6)),
+                        D=int(g.choice([8, 64, 1000, 2048, 4096])),
+                        window=int(g.choice([1, 2, 5, 64, 128])),
+                        mode=str(g.choice(["z", "mean", "raw", "ema"])),
+                        na=int(g.integers(1, 9)), nb=int(g.integers(0, 9)),
+                        chunks=cuts, seed=int(g.integers(1 << 30))))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_online_cases(12),
+                         ids=lambda c: f"{c['mode']}-D{c['D']}-w{c['window']}")
+def test_score_tokens_random(E, case):
+    """Seeded mixes of batch, hidden width, window, smoothing, band sizes and
+    a random cut of the stream into calls of 1..64 tokens: the fused scorer
+    bitwise equal to the two separate calls, and both equal to the oracle's
+    float64 scores of the whole stream."""
+    print(f"fused per-token scoring, random: {case}", flush=True)
+    g = np.random.default_rng(case["seed"])
+    B, D, T = case["B"], case["D"], sum(case["chunks"])
+    na, nb = case["na"], case["nb"]
+    scale = np.exp(g.normal(0.0, 0.5, size=(na + nb, 1, T, 1)))
+    hid = synth.f32_to_bf16_bits(
+        (g.standard_normal((na + nb, B, T, D)) * scale).astype(np.float32))
+    smode = {"z": E.SMOOTH_Z, "mean": E.SMOOTH_MEAN, "raw": E.SMOOTH_RAW,
+             "ema": E.SMOOTH_EMA}[case["mode"]]
+    cfg = E.default_cfg(batch=B, hidden=D, n_band_a=na, n_band_b=nb,
+                        smoothing=smode, window=case["window"])
+    assert E.check_cfg(cfg) == 0
+    a = _score_stream(E, cfg, hid, case["chunks"])
+    f = _score_stream(E, cfg, hid, case["chunks"], fused=True)
+    assert a[0].tobytes() == f[0].tobytes()
+    assert a[1].tobytes() == f[1].tobytes()
+    ref = _oracle_stream(hid, na, nb, case["mode"], case["window"])
+    tol = TOL if case["mode"] != "ema" else 1e-3
+    assert rel_err(f[0], ref, NEAR_ZERO) <= tol
