@@ -332,13 +332,11 @@ size_t epikv_select_workspace_bytes(const epikv_cfg* cfg);
  * workspace: epikv_select_workspace_bytes(cfg) bytes of device memory,
  * 16-byte aligned (EPIKV_EALIGN), overlapping none of the other arguments
  * (EPIKV_EALIAS); EPIKV_EWORKSPACE if it is missing or too small (it may be
- * NULL when that size is 0).  Between calls it carries the selection's
- * cleared scratch, so that no clearing launch is needed: reuse it unchanged
- * from one call to the next.  Any contents are accepted (a first use, or
- * scratch changed in between, is recognised by a 64-bit marker; that call
- * runs one workgroup per sequence and leaves the scratch cleared), and the
- * call may be captured in a HIP graph.  Calls that share a workspace must
- * not overlap in time.  Other arguments and errors as for epikv_select.
+ * NULL when that size is 0).  Any contents are accepted: a small fill
+ * kernel clears the scratch at the start of every split call, so nothing
+ * depends on what the memory held before, and the call may be captured in
+ * a HIP graph.  Calls that share a workspace must not overlap in time.
+ * Other arguments and errors as for epikv_select.
  */
 int epikv_select_ws(const epikv_cfg* cfg, const float* scores, int64_t ld_s,
                     const int32_t* n_cached, const int32_t* n_prefix,
@@ -514,9 +512,10 @@ int epikv_evict_step(const epikv_cfg* cfg, const epikv_step_io* io,
  * capture.  `stream` must belong to the calling thread's current device
  * (else EPIKV_EINVAL_PARAM); the address lookup failing returns
  * EPIKV_ELAUNCH.  Every call on one GPU shares its array, which keeps the
- * last call's contents (the step writes what it reads, apart from the
- * selection's scratch, which each call leaves cleared for the next): calls that overlap in time on one GPU -- on two streams, or
- * from two threads -- race and must not be issued.
+ * last call's contents (the step writes everything it reads from it, the
+ * selection's scratch through a clearing kernel): calls that overlap in
+ * time on one GPU -- on two streams, or from two threads -- race and must
+ * not be issued.
  */
 int epikv_evict_step_noalloc(const epikv_cfg* cfg, const epikv_step_io* io,
                              hipStream_t stream);

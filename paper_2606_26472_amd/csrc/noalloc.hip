@@ -11,10 +11,9 @@
 // current, and kept in `g_scratch`.  Only that address is ever handed to a
 // kernel.  Every call on one GPU shares the array and it keeps the last
 // call's contents; the step's kernels write every scratch word before they
-// read it, except the selection's histograms, which each call leaves
-// cleared for the next (recognised by a marker; the array starts zeroed,
-// without the marker, so the first call on a device clears them itself).  Calls that overlap in time on one GPU
-// (two streams, two threads) race on it.
+// read it (the selection's histograms are cleared by a fill kernel at the
+// start of each call).  Calls that overlap in time on one GPU (two
+// streams, two threads) race on it.
 #include <mutex>
 
 #include "epikv_internal.h"

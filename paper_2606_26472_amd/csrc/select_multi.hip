@@ -32,14 +32,15 @@
 // at zero and only grows towards its final value, a read whose words add up
 // to the known total has every word final.
 //
-// Each sequence's scratch therefore has to be clear when the kernel starts,
-// and no separate clearing launch is spent on it: a call leaves it clear
-// (each workgroup zeroes its share of the histograms once the output counts
-// show that every workgroup is past them, and its own count slot when it
-// starts), and a 64-bit marker says that it is.  Scratch without the
-// marker (first use of a workspace, or left by a call that gave up) is
-// cleared by the sequence's last workgroup, which then sets the marker,
-// while the others wait for it.
+// Each sequence's scratch therefore has to be clear when the kernel starts.
+// A small fill kernel launched just before it writes every sequence's block
+// (histograms and flags zero, a 64-bit marker that the block is clear), so
+// nothing depends on what the workspace held before: it may have served
+// another batch size's layout, or other data, since the previous call.
+// (Each workgroup also zeroes its own count slot when it starts and its
+// share of the histograms once every workgroup is past them; and a block
+// found without the marker is cleared by the sequence's last workgroup,
+// which then sets it, while the others wait.)
 //
 // The launcher keeps the grid within one workgroup per compute unit, so all
 // of a sequence's workgroups can run together; should they not (other work
@@ -509,6 +510,16 @@ int device_cus() {
 
 constexpr size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
+// Every sequence's scratch block made clear before the selection: head
+// words zero but for the marker, histograms zero.  One thread per word of
+// the first n_words words (the B sequences' blocks).
+__global__ __launch_bounds__(256) void k_select_scratch_clear(uint32_t* scratch, int64_t n_words) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_words) return;
+  const int64_t w = i % kSelSeqWords;
+  scratch[i] = w == 0 ? kSelMarkLo : (w == 1 ? kSelMarkHi : 0u);
+}
+
 }  // namespace
 
 size_t select_scratch_bytes(int B) {
@@ -535,6 +546,16 @@ hipError_t launch_select_groups(const SelectArgs& a, void* scratch, hipStream_t 
     }
   }
   if (v < 0) return launch_select(a, s);
+
+  // The scratch is cleared here rather than trusted to be as the previous
+  // call left it: a workspace may have held other data since (another
+  // batch size's layout, or the caller's own use), and a stale count would
+  // leave a histogram that never adds up.
+  const int64_t n_words = (int64_t)a.B * kSelSeqWords;
+  hipLaunchKernelGGL(k_select_scratch_clear, dim3((unsigned)((n_words + 255) / 256)), dim3(256), 0, s,
+                     (uint32_t*)scratch, n_words);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
 
   SelectMultiArgs m;
   m.sel = a;

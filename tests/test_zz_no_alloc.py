@@ -122,6 +122,30 @@ def _run(E, h, noalloc, mode):
     return {k: host(v).tobytes() for k, v in out.items()}, host(status)
 
 
+def test_noalloc_call_sequence_of_changing_shapes(E):
+    """Eight calls in a row on the one scratch array, each with another
+    layout of it: batch sizes that grow as well as shrink (sequences whose
+    selection scratch the previous call used for other data), chunks,
+    budgets, signals and rebuild modes; each equal to the step on fresh
+    workspace."""
+    g = np.random.default_rng(20261209)
+    for i in range(8):
+        B = int(g.choice([1, 2, 3, 5, 8, 13]))
+        C = int(g.choice([1, 16, 64]))
+        K = int(g.choice([64, 256, 512]))
+        n_max = int(max(C + 2, min(16000 // B, 4000)))
+        signal = str(g.choice(["hs", "lagkv"]))
+        mode = str(g.choice(["out_of_place", "remap"]))
+        print(f"no-alloc call {i}: {signal} {mode} B={B} C={C} K={K} "
+              f"n_max={n_max}", flush=True)
+        h = _inputs(E, g, signal, B, C, K, n_max)
+        ref, st_ref = _run(E, h, False, mode)
+        got, _ = _run(E, h, True, mode)
+        assert np.all(st_ref == 0), st_ref
+        for k in ref:
+            assert got[k] == ref[k], (i, k)
+
+
 @pytest.mark.parametrize("signal,mode", [("hs", "out_of_place"),
                                          ("lagkv", "out_of_place"),
                                          ("hs", "remap")])
