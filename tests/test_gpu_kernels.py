@@ -592,3 +592,41 @@ def _random_select_shapes(n, seed=20261206):
 @pytest.mark.parametrize("B,ld_s,K", _random_select_shapes(10))
 def test_select_split_random_shapes(E, B, ld_s, K):
     test_select_split_matches_oracle_bit_exact(E, B, ld_s, K)
+
+
+def test_select_split_ignores_stale_workspace(E):
+    """epikv_select_ws accepts any workspace contents: here every word but
+    each sequence's clear-marker is overwritten with garbage between two
+    calls (what another layout's data can leave), and the second call must
+    still be exact."""
+    import torch
+    B, ld_s, K = 3, 40000, 1024
+    g = synth.rng(911)
+    Ns = g.integers(K + 1, ld_s + 1, B)
+    Ps = g.integers(0, K // 8, B)
+    sc = np.stack([synth.old_scores(g, ld_s, ties=True) for _ in range(B)])
+    cfg = E.default_cfg(batch=B, budget=K)
+    n = E.select_workspace_bytes(cfg)
+    assert n > 0
+    ws = torch.zeros(n // 4, dtype=torch.int32, device="cuda")
+    d_sc, d_n, d_p = dev(sc), dev(Ns.astype(np.int32)), dev(Ps.astype(np.int32))
+    R = O.default_recent(K)
+    for rep in range(2):
+        keep = torch.full((B, K), -5, dtype=torch.int32, device="cuda")
+        nk = torch.zeros(B, dtype=torch.int32, device="cuda")
+        st = torch.full((B,), 9, dtype=torch.int32, device="cuda")
+        E.epikv_select_ws(cfg, d_sc, ld_s, d_n, d_p, keep, nk, st, ws, n)
+        _sync()
+        kh, nh, sh = host(keep), host(nk), host(st)
+        for b in range(B):
+            ref = O.select_keep(sc[b, :Ns[b]], int(Ps[b]), K, R)
+            assert sh[b] == E.SEQ_OK and nh[b] == ref.size, (rep, b)
+            assert np.array_equal(kh[b, :ref.size], ref), (rep, b)
+        # garbage everywhere except the first two words of every block
+        words = ws.cpu().numpy()
+        marks = words.copy()
+        words[:] = 0x11111111
+        seq_words = 6208                 # words per sequence block (24832 bytes)
+        for b in range(B):
+            words[b * seq_words:b * seq_words + 2] = marks[b * seq_words:b * seq_words + 2]
+        ws.copy_(torch.from_numpy(words))
